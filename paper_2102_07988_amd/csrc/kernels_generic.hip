@@ -1,0 +1,413 @@
+// Generic kernels of the stage: a strided tiled-FMA GEMM with the fused
+// epilogues, straightforward prefix-causal attention forward/backward (one
+// block per (query, head)), LayerNorm forward/backward, column reductions.
+// These carry the fp32 validation mode and every shape the bf16 fast kernels
+// do not take.
+#include "tp_common.hpp"
+#include "tp_kernels.hpp"
+
+namespace tp {
+
+// ------------------------------------------------------------------ epilogue
+
+template <typename T, int EPI>
+__device__ inline void gemm_epilogue(const GemmArgs& a, int m, int n, float acc) {
+  if constexpr (EPI == EPI_ACC_F32) {
+    float* C = (float*)a.C + (long)m * a.ldc + n;
+    *C += acc;
+  } else if constexpr (EPI == EPI_DGELU) {
+    const float z = ld((const T*)a.R + (long)m * a.ldr + n);
+    st((T*)a.C + (long)m * a.ldc + n, acc * gelu_tanh_grad(z));
+  } else {
+    const float v = acc + (a.bias ? ld((const T*)a.bias + n) : 0.f);
+    if constexpr (EPI == EPI_STORE) {
+      st((T*)a.C + (long)m * a.ldc + n, v);
+    } else if constexpr (EPI == EPI_RESID) {
+      st((T*)a.C + (long)m * a.ldc + n, v + ld((const T*)a.R + (long)m * a.ldr + n));
+    } else if constexpr (EPI == EPI_GELU) {
+      st((T*)a.C + (long)m * a.ldc + n, v);
+      st((T*)a.C2 + (long)m * a.ldc2 + n, gelu_tanh(v));
+    } else if constexpr (EPI == EPI_QKV) {
+      const int H = a.H;
+      if (n < H)
+        st((T*)a.q + (long)m * H + n, v);
+      else if (n < 2 * H)
+        st((T*)a.k + (long)m * H + (n - H), v);
+      else
+        st((T*)a.v + (long)m * H + (n - 2 * H), v);
+    }
+  }
+}
+
+// ------------------------------------------------------------- generic GEMM
+
+template <typename T, int EPI>
+__global__ __launch_bounds__(256) void gemm_generic_kernel(GemmArgs a) {
+  __shared__ float As[16][65];
+  __shared__ float Bs[16][65];
+  const T* A = (const T*)a.A;
+  const T* B = (const T*)a.B;
+  const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  // contiguous dimension of each operand decides the load order (coalescing)
+  const bool a_k_fast = a.sak == 1;
+  const bool b_n_fast = a.sbn == 1;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < a.K; k0 += 16) {
+    for (int e = threadIdx.x; e < 1024; e += 256) {
+      int kk, mm;
+      if (a_k_fast) {
+        kk = e & 15;
+        mm = e >> 4;
+      } else {
+        kk = e >> 6;
+        mm = e & 63;
+      }
+      const int gm = m0 + mm, gk = k0 + kk;
+      As[kk][mm] = (gm < a.M && gk < a.K) ? ld(A + (long)gm * a.sam + (long)gk * a.sak) : 0.f;
+      int kb, nn;
+      if (b_n_fast) {
+        kb = e >> 6;
+        nn = e & 63;
+      } else {
+        kb = e & 15;
+        nn = e >> 4;
+      }
+      const int gn = n0 + nn, gkb = k0 + kb;
+      Bs[kb][nn] = (gn < a.N && gkb < a.K) ? ld(B + (long)gkb * a.sbk + (long)gn * a.sbn) : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float av[4], bv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) av[i] = As[kk][ty + 16 * i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bv[j] = Bs[kk][tx + 16 * j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] += av[i] * bv[j];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int m = m0 + ty + 16 * i, n = n0 + tx + 16 * j;
+      if (m < a.M && n < a.N) gemm_epilogue<T, EPI>(a, m, n, acc[i][j]);
+    }
+}
+
+template <typename T>
+static hipError_t gemm_generic_t(const GemmArgs& a, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  dim3 grid(cdiv(a.N, 64), cdiv(a.M, 64));
+  switch (a.epi) {
+    case EPI_STORE: gemm_generic_kernel<T, EPI_STORE><<<grid, 256, 0, s>>>(a); break;
+    case EPI_QKV: gemm_generic_kernel<T, EPI_QKV><<<grid, 256, 0, s>>>(a); break;
+    case EPI_RESID: gemm_generic_kernel<T, EPI_RESID><<<grid, 256, 0, s>>>(a); break;
+    case EPI_GELU: gemm_generic_kernel<T, EPI_GELU><<<grid, 256, 0, s>>>(a); break;
+    case EPI_DGELU: gemm_generic_kernel<T, EPI_DGELU><<<grid, 256, 0, s>>>(a); break;
+    case EPI_ACC_F32: gemm_generic_kernel<T, EPI_ACC_F32><<<grid, 256, 0, s>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t gemm_generic(int dtype, const GemmArgs& a, hipStream_t s) {
+  return dtype == DT_FP32 ? gemm_generic_t<float>(a, s) : gemm_generic_t<bf16>(a, s);
+}
+
+// ------------------------------------------------------- generic attention
+
+// One block per (query row, head).  LDS: scores [Lmax] (+ dP [Lmax] for bwd),
+// q and dO rows, reduction scratch.
+template <typename T>
+__global__ __launch_bounds__(256) void attn_fwd_generic_kernel(AttnArgs a) {
+  extern __shared__ float sm[];
+  const int i = blockIdx.x, t = a.l + i, h = blockIdx.y, d = a.d, H = a.H;
+  float* S = sm;
+  float* qs = sm + a.Lmax;
+  float* red = qs + 128;
+  const T* q = (const T*)a.q + (long)i * H + h * d;
+  for (int j = threadIdx.x; j < d; j += blockDim.x) qs[j] = ld(q + j);
+  __syncthreads();
+  float mx = -INFINITY;
+  for (int s = threadIdx.x; s <= t; s += blockDim.x) {
+    const T* k = (const T*)a.kc + (long)s * H + h * d;
+    float dot = 0.f;
+    for (int j = 0; j < d; ++j) dot += qs[j] * ld(k + j);
+    dot *= a.scale;
+    S[s] = dot;
+    mx = fmaxf(mx, dot);
+  }
+  mx = block_max(mx, red);
+  float sum = 0.f;
+  for (int s = threadIdx.x; s <= t; s += blockDim.x) {
+    const float e = __expf(S[s] - mx);
+    S[s] = e;
+    sum += e;
+  }
+  sum = block_sum(sum, red);
+  const float inv = 1.f / sum;
+  for (int j = threadIdx.x; j < d; j += blockDim.x) {
+    float acc = 0.f;
+    for (int s = 0; s <= t; ++s) acc += S[s] * ld((const T*)a.vc + (long)s * H + h * d + j);
+    st((T*)a.o + (long)i * H + h * d + j, acc * inv);
+  }
+  if (threadIdx.x == 0) a.lse[(long)h * a.Lmax + t] = mx + logf(sum);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void attn_bwd_generic_kernel(AttnArgs a) {
+  extern __shared__ float sm[];
+  const int i = blockIdx.x, t = a.l + i, h = blockIdx.y, d = a.d, H = a.H;
+  float* P = sm;
+  float* dS = sm + a.Lmax;
+  float* qs = dS + a.Lmax;
+  float* ds_ = qs + 128;
+  float* red = ds_ + 128;
+  for (int j = threadIdx.x; j < d; j += blockDim.x) {
+    qs[j] = ld((const T*)a.q + (long)i * H + h * d + j);
+    ds_[j] = ld((const T*)a.dout + (long)i * H + h * d + j);
+  }
+  __syncthreads();
+  const float lse = a.lse[(long)h * a.Lmax + t];
+  float Dp = 0.f;
+  for (int s = threadIdx.x; s <= t; s += blockDim.x) {
+    const T* k = (const T*)a.kc + (long)s * H + h * d;
+    const T* v = (const T*)a.vc + (long)s * H + h * d;
+    float dot = 0.f, dpv = 0.f;
+    for (int j = 0; j < d; ++j) {
+      dot += qs[j] * ld(k + j);
+      dpv += ds_[j] * ld(v + j);
+    }
+    const float p = __expf(dot * a.scale - lse);
+    P[s] = p;
+    dS[s] = dpv;
+    Dp += p * dpv;
+  }
+  const float D = block_sum(Dp, red);
+  for (int s = threadIdx.x; s <= t; s += blockDim.x) dS[s] = P[s] * (dS[s] - D);
+  __syncthreads();
+  for (int j = threadIdx.x; j < d; j += blockDim.x) {
+    float acc = 0.f;
+    for (int s = 0; s <= t; ++s) acc += dS[s] * ld((const T*)a.kc + (long)s * H + h * d + j);
+    st((T*)a.dq + (long)i * a.ld_dq + h * d + j, acc * a.scale);
+  }
+  const long tot = (long)(t + 1) * d;
+  for (long e = threadIdx.x; e < tot; e += blockDim.x) {
+    const int s = (int)(e / d), j = (int)(e % d);
+    atomicAdd(a.dk + (long)s * H + h * d + j, dS[s] * qs[j] * a.scale);
+    atomicAdd(a.dv + (long)s * H + h * d + j, P[s] * ds_[j]);
+  }
+}
+
+template <typename T>
+static hipError_t attn_generic_t(const AttnArgs& a, bool bwd, hipStream_t s) {
+  const size_t lds = bwd ? (2 * (size_t)a.Lmax + 256 + 16) * 4 : ((size_t)a.Lmax + 128 + 16) * 4;
+  if (lds > 160 * 1024) return hipErrorInvalidValue;
+  if (lds > 64 * 1024) {
+    const void* fn = bwd ? (const void*)attn_bwd_generic_kernel<T>
+                         : (const void*)attn_fwd_generic_kernel<T>;
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  dim3 grid(a.r - a.l, a.heads);
+  if (bwd)
+    attn_bwd_generic_kernel<T><<<grid, 256, lds, s>>>(a);
+  else
+    attn_fwd_generic_kernel<T><<<grid, 256, lds, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t attn_fwd_generic(int dtype, const AttnArgs& a, hipStream_t s) {
+  return dtype == DT_FP32 ? attn_generic_t<float>(a, false, s) : attn_generic_t<bf16>(a, false, s);
+}
+hipError_t attn_bwd_generic(int dtype, const AttnArgs& a, hipStream_t s) {
+  return dtype == DT_FP32 ? attn_generic_t<float>(a, true, s) : attn_generic_t<bf16>(a, true, s);
+}
+
+// ------------------------------------------------------------- LayerNorm
+
+template <typename T>
+__global__ __launch_bounds__(256) void ln_fwd_kernel(int H, const T* x, T* x_copy, const T* g,
+                                                     const T* b, T* u, float* mean, float* rstd,
+                                                     float eps) {
+  __shared__ float red[16];
+  const int row = blockIdx.x;
+  const T* xr = x + (long)row * H;
+  float s = 0.f;
+  for (int i = threadIdx.x; i < H; i += blockDim.x) s += ld(xr + i);
+  const float mu = block_sum(s, red) / H;
+  float v = 0.f;
+  for (int i = threadIdx.x; i < H; i += blockDim.x) {
+    const float c = ld(xr + i) - mu;
+    v += c * c;
+  }
+  const float rs = rsqrtf(block_sum(v, red) / H + eps);
+  for (int i = threadIdx.x; i < H; i += blockDim.x) {
+    const float xv = ld(xr + i);
+    st(u + (long)row * H + i, ld(g + i) * ((xv - mu) * rs) + ld(b + i));
+    if (x_copy) x_copy[(long)row * H + i] = xr[i];
+  }
+  if (threadIdx.x == 0) {
+    mean[row] = mu;
+    rstd[row] = rs;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void ln_bwd_kernel(int H, const T* du, const T* x,
+                                                     const float* mean, const float* rstd,
+                                                     const T* g, const T* resid, T* dx) {
+  __shared__ float red[16];
+  const int row = blockIdx.x;
+  const float mu = mean[row], rs = rstd[row];
+  float sa = 0.f, sb = 0.f;
+  for (int i = threadIdx.x; i < H; i += blockDim.x) {
+    const float xh = (ld(x + (long)row * H + i) - mu) * rs;
+    const float dxh = ld(du + (long)row * H + i) * ld(g + i);
+    sa += dxh;
+    sb += dxh * xh;
+  }
+  const float a = block_sum(sa, red) / H;
+  const float b = block_sum(sb, red) / H;
+  for (int i = threadIdx.x; i < H; i += blockDim.x) {
+    const float xh = (ld(x + (long)row * H + i) - mu) * rs;
+    float v = rs * (ld(du + (long)row * H + i) * ld(g + i) - a - xh * b);
+    if (resid) v += ld(resid + (long)row * H + i);
+    st(dx + (long)row * H + i, v);
+  }
+}
+
+// Column reductions: each block owns 256 consecutive columns and loops over
+// all rows in order, so results are deterministic.
+template <typename T>
+__global__ __launch_bounds__(256) void ln_param_grads_kernel(int n, int H, const T* du,
+                                                             const T* x, const float* mean,
+                                                             const float* rstd, float* dg,
+                                                             float* db) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= H) return;
+  float sg = 0.f, sb = 0.f;
+  for (int t = 0; t < n; ++t) {
+    const float d = ld(du + (long)t * H + i);
+    sg += d * ((ld(x + (long)t * H + i) - mean[t]) * rstd[t]);
+    sb += d;
+  }
+  dg[i] += sg;
+  db[i] += sb;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void colsum_kernel(int n, int N, const T* A, long lda,
+                                                     float* out) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= N) return;
+  float s = 0.f;
+  for (int t = 0; t < n; ++t) s += ld(A + (long)t * lda + j);
+  out[j] += s;
+}
+
+template <typename T>
+__global__ void pack_dkv_kernel(int n, int H, const float* dk, const float* dv, T* dqkv) {
+  const long e = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= (long)n * H) return;
+  const long i = e / H, j = e % H;
+  st(dqkv + i * 3 * H + H + j, dk[e]);
+  st(dqkv + i * 3 * H + 2 * H + j, dv[e]);
+}
+
+__global__ void fill_f32_kernel(float* p, size_t n, float v) {
+  for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
+       e += (size_t)gridDim.x * blockDim.x)
+    p[e] = v;
+}
+
+template <typename T>
+__global__ void copy_kernel(size_t n, const T* src, T* dst) {
+  for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
+       e += (size_t)gridDim.x * blockDim.x)
+    dst[e] = src[e];
+}
+
+hipError_t ln_fwd(int dtype, int n, int H, const void* x, void* x_copy, const void* g,
+                  const void* b, void* u, float* mean, float* rstd, float eps, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (dtype == DT_FP32)
+    ln_fwd_kernel<float><<<n, 256, 0, s>>>(H, (const float*)x, (float*)x_copy, (const float*)g,
+                                           (const float*)b, (float*)u, mean, rstd, eps);
+  else
+    ln_fwd_kernel<bf16><<<n, 256, 0, s>>>(H, (const bf16*)x, (bf16*)x_copy, (const bf16*)g,
+                                          (const bf16*)b, (bf16*)u, mean, rstd, eps);
+  return hipGetLastError();
+}
+
+hipError_t ln_bwd(int dtype, int n, int H, const void* du, const void* x, const float* mean,
+                  const float* rstd, const void* g, const void* resid, void* dx, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (dtype == DT_FP32)
+    ln_bwd_kernel<float><<<n, 256, 0, s>>>(H, (const float*)du, (const float*)x, mean, rstd,
+                                           (const float*)g, (const float*)resid, (float*)dx);
+  else
+    ln_bwd_kernel<bf16><<<n, 256, 0, s>>>(H, (const bf16*)du, (const bf16*)x, mean, rstd,
+                                          (const bf16*)g, (const bf16*)resid, (bf16*)dx);
+  return hipGetLastError();
+}
+
+hipError_t ln_param_grads(int dtype, int n, int H, const void* du, const void* x,
+                          const float* mean, const float* rstd, float* dg, float* db,
+                          hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (dtype == DT_FP32)
+    ln_param_grads_kernel<float><<<cdiv(H, 256), 256, 0, s>>>(n, H, (const float*)du,
+                                                               (const float*)x, mean, rstd, dg, db);
+  else
+    ln_param_grads_kernel<bf16><<<cdiv(H, 256), 256, 0, s>>>(n, H, (const bf16*)du,
+                                                              (const bf16*)x, mean, rstd, dg, db);
+  return hipGetLastError();
+}
+
+hipError_t colsum_acc(int dtype, int n, int N, const void* A, long lda, float* out,
+                      hipStream_t s) {
+  if (n <= 0 || N <= 0) return hipSuccess;
+  if (dtype == DT_FP32)
+    colsum_kernel<float><<<cdiv(N, 256), 256, 0, s>>>(n, N, (const float*)A, lda, out);
+  else
+    colsum_kernel<bf16><<<cdiv(N, 256), 256, 0, s>>>(n, N, (const bf16*)A, lda, out);
+  return hipGetLastError();
+}
+
+hipError_t pack_dkv(int dtype, int n, int H, const float* dk, const float* dv, void* dqkv,
+                    hipStream_t s) {
+  const long tot = (long)n * H;
+  if (tot <= 0) return hipSuccess;
+  if (dtype == DT_FP32)
+    pack_dkv_kernel<float><<<cdiv(tot, 256), 256, 0, s>>>(n, H, dk, dv, (float*)dqkv);
+  else
+    pack_dkv_kernel<bf16><<<cdiv(tot, 256), 256, 0, s>>>(n, H, dk, dv, (bf16*)dqkv);
+  return hipGetLastError();
+}
+
+hipError_t fill_f32(float* p, size_t n, float v, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const int blocks = (int)((n + 255) / 256 < 8192 ? (n + 255) / 256 : 8192);
+  fill_f32_kernel<<<blocks, 256, 0, s>>>(p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t copy_rows(int dtype, int n, int H, const void* src, void* dst, hipStream_t s) {
+  const size_t tot = (size_t)n * H;
+  if (tot == 0) return hipSuccess;
+  const int blocks = (int)((tot + 255) / 256 < 8192 ? (tot + 255) / 256 : 8192);
+  if (dtype == DT_FP32)
+    copy_kernel<float><<<blocks, 256, 0, s>>>(tot, (const float*)src, (float*)dst);
+  else
+    copy_kernel<bf16><<<blocks, 256, 0, s>>>(tot, (const bf16*)src, (bf16*)dst);
+  return hipGetLastError();
+}
+
+}  // namespace tp

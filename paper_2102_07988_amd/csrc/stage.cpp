@@ -1,0 +1,584 @@
+// Stage engine behind the C ABI of include/terapipe.h: workspace layout, the
+// slice state machine (cached length / backward frontier), the per-layer
+// launch sequences of a slice's forward and backward, the deferred
+// weight-gradient pass, the slice-cost profiler and per-kernel timing.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "tp_common.hpp"
+#include "tp_kernels.hpp"
+
+using namespace tp;
+
+namespace {
+
+struct LayerBufs {
+  // per-token activation arena, rows are absolute token positions
+  void *x_in, *u, *q, *kc, *vc, *o, *x1, *u2, *z, *g;
+  float *mean1, *rstd1, *mean2, *rstd2;
+  float* lse;     // [heads][Lmax]
+  float *dk, *dv; // fp32 [Lmax][H]: gradient reaching each cached key / value
+  // per-token output gradients of the four projections (inputs of dW GEMMs)
+  void *dy, *dz, *dx1, *dqkv;
+};
+
+struct Scratch {
+  void *du2, *du, *dout;  // [Lmax][H]
+  float* D;               // [heads][Lmax]
+  void *io_a, *io_b;      // profiler slice buffers [Lmax][H]
+};
+
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base((char*)b) {}
+  void* take(size_t bytes) {
+    off = (off + 255) & ~(size_t)255;
+    void* p = base ? base + off : nullptr;
+    off += bytes;
+    return p;
+  }
+};
+
+enum KClass { K_GEMM_FWD, K_GEMM_DX, K_GEMM_DW, K_ATTN_FWD, K_ATTN_BWD, K_NORM, K_MISC, K_N };
+const char* kclass_name[K_N] = {"gemm_fwd_nt", "gemm_bwd_dx_nn", "gemm_bwd_dw_tn", "attn_fwd",
+                                "attn_bwd",    "layernorm",      "misc"};
+
+struct PendingTiming {
+  int cls;
+  hipEvent_t a, b;
+  double flops, bytes;
+};
+
+}  // namespace
+
+struct tp_stage {
+  tp_stage_config cfg;
+  int H, F, heads, d, L, dt;
+  size_t esz;
+  std::vector<tp_layer_ptrs> P, G;
+  std::vector<LayerBufs> lb;
+  Scratch sc;
+  hipStream_t stream;
+  int cached_len = 0, bwd_frontier = 0;
+  bool profiling = false;
+  // timing
+  bool timing = false;
+  std::vector<PendingTiming> pending;
+  std::vector<hipEvent_t> free_events;
+  int64_t launches[K_N] = {};
+  double total_ms[K_N] = {}, flops[K_N] = {}, bytes[K_N] = {};
+};
+
+namespace {
+
+bool config_ok(const tp_stage_config* c) {
+  if (!c) return false;
+  if (c->n_layers < 1 || c->n_layers > 1024 || c->hidden < 1 || c->heads < 1 || c->max_seq < 1)
+    return false;
+  if (c->hidden % c->heads) return false;
+  if (c->dtype != TP_DTYPE_BF16 && c->dtype != TP_DTYPE_FP32) return false;
+  if (c->wgrad_mode != TP_WGRAD_PER_SLICE && c->wgrad_mode != TP_WGRAD_DEFERRED) return false;
+  if (!(c->ln_eps > 0.f) || !std::isfinite(c->ln_eps)) return false;
+  return true;
+}
+
+bool config_supported(const tp_stage_config* c) {
+  const int d = c->hidden / c->heads;
+  if (d != 16 && d != 32 && d != 64 && d != 128) return false;
+  if (c->hidden % 8) return false;
+  // the generic attention keeps one score row per block in LDS
+  if ((2 * (size_t)c->max_seq + 272) * 4 > 160 * 1024) return false;
+  return true;
+}
+
+size_t carve(const tp_stage_config* c, void* base, std::vector<LayerBufs>* lbs, Scratch* sc) {
+  Carver cv(base);
+  const size_t esz = c->dtype == TP_DTYPE_FP32 ? 4 : 2;
+  const size_t L = c->max_seq, H = c->hidden, F = 4 * H, a = c->heads;
+  for (int i = 0; i < c->n_layers; ++i) {
+    LayerBufs b;
+    b.x_in = cv.take(L * H * esz);
+    b.u = cv.take(L * H * esz);
+    b.q = cv.take(L * H * esz);
+    b.kc = cv.take(L * H * esz);
+    b.vc = cv.take(L * H * esz);
+    b.o = cv.take(L * H * esz);
+    b.x1 = cv.take(L * H * esz);
+    b.u2 = cv.take(L * H * esz);
+    b.z = cv.take(L * F * esz);
+    b.g = cv.take(L * F * esz);
+    b.mean1 = (float*)cv.take(L * 4);
+    b.rstd1 = (float*)cv.take(L * 4);
+    b.mean2 = (float*)cv.take(L * 4);
+    b.rstd2 = (float*)cv.take(L * 4);
+    b.lse = (float*)cv.take(a * L * 4);
+    b.dk = (float*)cv.take(L * H * 4);
+    b.dv = (float*)cv.take(L * H * 4);
+    b.dy = cv.take(L * H * esz);
+    b.dz = cv.take(L * F * esz);
+    b.dx1 = cv.take(L * H * esz);
+    b.dqkv = cv.take(L * 3 * H * esz);
+    if (lbs) lbs->push_back(b);
+  }
+  Scratch s;
+  s.du2 = cv.take(L * H * esz);
+  s.du = cv.take(L * H * esz);
+  s.dout = cv.take(L * H * esz);
+  s.D = (float*)cv.take(a * L * 4);
+  s.io_a = cv.take(L * H * esz);
+  s.io_b = cv.take(L * H * esz);
+  if (sc) *sc = s;
+  return (cv.off + 255) & ~(size_t)255;
+}
+
+inline void* rowp(void* p, long t, long width, size_t esz) { return (char*)p + t * width * esz; }
+inline const void* rowp(const void* p, long t, long width, size_t esz) {
+  return (const char*)p + t * width * esz;
+}
+
+hipEvent_t get_event(tp_stage* S) {
+  if (!S->free_events.empty()) {
+    hipEvent_t e = S->free_events.back();
+    S->free_events.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Run one launch, bracketed by events when timing is on.
+template <typename Fn>
+hipError_t launch(tp_stage* S, int cls, double flops, double bytes, Fn&& fn) {
+  if (!S->timing) return fn();
+  hipEvent_t a = get_event(S), b = get_event(S);
+  if (!a || !b) return hipErrorOutOfMemory;
+  hipEventRecord(a, S->stream);
+  hipError_t e = fn();
+  hipEventRecord(b, S->stream);
+  S->pending.push_back({cls, a, b, flops, bytes});
+  return e;
+}
+
+#define TRY(expr)                             \
+  do {                                        \
+    hipError_t _e = (expr);                   \
+    if (_e != hipSuccess) return TP_ERR_HIP;  \
+  } while (0)
+
+double gemm_bytes(const GemmArgs& g, size_t esz) {
+  double b = ((double)g.M * g.K + (double)g.K * g.N) * esz;
+  if (g.epi == EPI_ACC_F32)
+    b += 8.0 * g.M * g.N;
+  else
+    b += (double)g.M * g.N * esz * (g.epi == EPI_GELU ? 2 : 1) +
+         (g.epi == EPI_RESID || g.epi == EPI_DGELU ? (double)g.M * g.N * esz : 0.0);
+  return b;
+}
+
+hipError_t run_gemm(tp_stage* S, int cls, const GemmArgs& g) {
+  return launch(S, cls, 2.0 * g.M * g.N * g.K, gemm_bytes(g, S->esz),
+                [&] { return gemm(S->dt, g, S->stream); });
+}
+
+// A(m,k) row-major [M][K] times weight W [N][K] (B(k,n) = W[n][k]).
+GemmArgs nt(int M, int N, int K, const void* A, long lda, const void* W) {
+  GemmArgs g;
+  g.M = M, g.N = N, g.K = K;
+  g.A = A, g.sam = lda, g.sak = 1;
+  g.B = W, g.sbk = 1, g.sbn = K;
+  return g;
+}
+// dX = dY [M][K] times W [K][N] (W stored [out = K][in = N]).
+GemmArgs nn(int M, int N, int K, const void* A, long lda, const void* W) {
+  GemmArgs g;
+  g.M = M, g.N = N, g.K = K;
+  g.A = A, g.sam = lda, g.sak = 1;
+  g.B = W, g.sbk = N, g.sbn = 1;
+  return g;
+}
+// dW [M][N] += sum over K tokens of dY[t][m] X[t][n].
+GemmArgs tn(int M, int N, int K, const void* dY, long ldy, const void* X, long ldx, float* dW) {
+  GemmArgs g;
+  g.M = M, g.N = N, g.K = K;
+  g.A = dY, g.sam = 1, g.sak = ldy;
+  g.B = X, g.sbk = ldx, g.sbn = 1;
+  g.epi = EPI_ACC_F32;
+  g.C = dW, g.ldc = N;
+  return g;
+}
+
+tp_status wgrad_gemms(tp_stage* S, int li, int l, int n) {
+  const int H = S->H, F = S->F;
+  const size_t e = S->esz;
+  LayerBufs& B = S->lb[li];
+  tp_layer_ptrs& G = S->G[li];
+  TRY(run_gemm(S, K_GEMM_DW, tn(H, F, n, rowp(B.dy, l, H, e), H, rowp(B.g, l, F, e), F,
+                                (float*)G.w_fc2)));
+  TRY(run_gemm(S, K_GEMM_DW, tn(F, H, n, rowp(B.dz, l, F, e), F, rowp(B.u2, l, H, e), H,
+                                (float*)G.w_fc1)));
+  TRY(run_gemm(S, K_GEMM_DW, tn(H, H, n, rowp(B.dx1, l, H, e), H, rowp(B.o, l, H, e), H,
+                                (float*)G.w_o)));
+  TRY(run_gemm(S, K_GEMM_DW, tn(3 * H, H, n, rowp(B.dqkv, l, 3 * H, e), 3 * H,
+                                rowp(B.u, l, H, e), H, (float*)G.w_qkv)));
+  return TP_OK;
+}
+
+tp_status forward_impl(tp_stage* S, int l, int r, const void* x, void* y) {
+  const int H = S->H, F = S->F, n = r - l, NL = S->cfg.n_layers, dt = S->dt;
+  const size_t e = S->esz;
+  hipStream_t st = S->stream;
+  const double nb = (double)n * H * e;
+  for (int li = 0; li < NL; ++li) {
+    LayerBufs& B = S->lb[li];
+    const tp_layer_ptrs& P = S->P[li];
+    void* xin = rowp(B.x_in, l, H, e);
+    TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
+      return ln_fwd(dt, n, H, li == 0 ? x : xin, li == 0 ? xin : nullptr, P.ln1_g, P.ln1_b,
+                    rowp(B.u, l, H, e), B.mean1 + l, B.rstd1 + l, S->cfg.ln_eps, st);
+    }));
+    GemmArgs g = nt(n, 3 * H, H, rowp(B.u, l, H, e), H, P.w_qkv);
+    g.epi = EPI_QKV;
+    g.bias = P.b_qkv;
+    g.q = rowp(B.q, l, H, e), g.k = rowp(B.kc, l, H, e), g.v = rowp(B.vc, l, H, e), g.H = H;
+    TRY(run_gemm(S, K_GEMM_FWD, g));
+    AttnArgs a;
+    a.l = l, a.r = r, a.H = H, a.heads = S->heads, a.d = S->d, a.Lmax = S->L;
+    a.scale = 1.f / std::sqrt((float)S->d);
+    a.q = rowp(B.q, l, H, e), a.kc = B.kc, a.vc = B.vc, a.o = rowp(B.o, l, H, e), a.lse = B.lse;
+    const double pairs = (double)n * l + (double)n * (n + 1) / 2;
+    TRY(launch(S, K_ATTN_FWD, 4.0 * H * pairs, (2.0 * n + 2.0 * r) * H * e,
+               [&] { return attn_fwd(dt, a, st); }));
+    g = nt(n, H, H, rowp(B.o, l, H, e), H, P.w_o);
+    g.epi = EPI_RESID, g.bias = P.b_o, g.R = xin, g.ldr = H, g.C = rowp(B.x1, l, H, e), g.ldc = H;
+    TRY(run_gemm(S, K_GEMM_FWD, g));
+    TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
+      return ln_fwd(dt, n, H, rowp(B.x1, l, H, e), nullptr, P.ln2_g, P.ln2_b,
+                    rowp(B.u2, l, H, e), B.mean2 + l, B.rstd2 + l, S->cfg.ln_eps, st);
+    }));
+    g = nt(n, F, H, rowp(B.u2, l, H, e), H, P.w_fc1);
+    g.epi = EPI_GELU, g.bias = P.b_fc1, g.C = rowp(B.z, l, F, e), g.ldc = F;
+    g.C2 = rowp(B.g, l, F, e), g.ldc2 = F;
+    TRY(run_gemm(S, K_GEMM_FWD, g));
+    g = nt(n, H, F, rowp(B.g, l, F, e), F, P.w_fc2);
+    g.epi = EPI_RESID, g.bias = P.b_fc2, g.R = rowp(B.x1, l, H, e), g.ldr = H;
+    g.C = li == NL - 1 ? y : rowp(S->lb[li + 1].x_in, l, H, e), g.ldc = H;
+    TRY(run_gemm(S, K_GEMM_FWD, g));
+  }
+  return TP_OK;
+}
+
+tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
+  const int H = S->H, F = S->F, n = r - l, NL = S->cfg.n_layers, dt = S->dt;
+  const size_t e = S->esz;
+  hipStream_t st = S->stream;
+  const bool per_slice = S->cfg.wgrad_mode == TP_WGRAD_PER_SLICE;
+  const double nb = (double)n * H * e;
+  for (int li = NL - 1; li >= 0; --li) {
+    LayerBufs& B = S->lb[li];
+    const tp_layer_ptrs& P = S->P[li];
+    tp_layer_ptrs& G = S->G[li];
+    void* dyl = rowp(B.dy, l, H, e);
+    if (li == NL - 1)
+      TRY(launch(S, K_MISC, 0, 2 * nb, [&] { return copy_rows(dt, n, H, dy, dyl, st); }));
+    // FC2 backward (dX fused with GELU'): dz = (dy W2) * GELU'(z)
+    GemmArgs g = nn(n, F, H, dyl, H, P.w_fc2);
+    g.epi = EPI_DGELU, g.R = rowp(B.z, l, F, e), g.ldr = F, g.C = rowp(B.dz, l, F, e), g.ldc = F;
+    TRY(run_gemm(S, K_GEMM_DX, g));
+    TRY(launch(S, K_MISC, 0, nb, [&] { return colsum_acc(dt, n, H, dyl, H, (float*)G.b_fc2, st); }));
+    // FC1 backward: du2 = dz W1
+    g = nn(n, H, F, rowp(B.dz, l, F, e), F, P.w_fc1);
+    g.C = S->sc.du2, g.ldc = H;
+    TRY(run_gemm(S, K_GEMM_DX, g));
+    TRY(launch(S, K_MISC, 0, (double)n * F * e, [&] {
+      return colsum_acc(dt, n, F, rowp(B.dz, l, F, e), F, (float*)G.b_fc1, st);
+    }));
+    // LN2 backward + residual: dx1 = dy + LN2^T(du2)
+    TRY(launch(S, K_NORM, 0, 4 * nb, [&] {
+      return ln_bwd(dt, n, H, S->sc.du2, rowp(B.x1, l, H, e), B.mean2 + l, B.rstd2 + l, P.ln2_g,
+                    dyl, rowp(B.dx1, l, H, e), st);
+    }));
+    TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
+      return ln_param_grads(dt, n, H, S->sc.du2, rowp(B.x1, l, H, e), B.mean2 + l, B.rstd2 + l,
+                            (float*)G.ln2_g, (float*)G.ln2_b, st);
+    }));
+    // output projection backward: dO = dx1 W_o
+    g = nn(n, H, H, rowp(B.dx1, l, H, e), H, P.w_o);
+    g.C = S->sc.dout, g.ldc = H;
+    TRY(run_gemm(S, K_GEMM_DX, g));
+    TRY(launch(S, K_MISC, 0, nb, [&] {
+      return colsum_acc(dt, n, H, rowp(B.dx1, l, H, e), H, (float*)G.b_o, st);
+    }));
+    // attention backward: dq rows, dK/dV into the fp32 buffer for keys [0, r)
+    AttnArgs a;
+    a.l = l, a.r = r, a.H = H, a.heads = S->heads, a.d = S->d, a.Lmax = S->L;
+    a.scale = 1.f / std::sqrt((float)S->d);
+    a.q = rowp(B.q, l, H, e), a.kc = B.kc, a.vc = B.vc, a.o = rowp(B.o, l, H, e), a.lse = B.lse;
+    a.dout = S->sc.dout, a.D = S->sc.D;
+    a.dq = rowp(B.dqkv, l, 3 * H, e), a.ld_dq = 3 * H;
+    a.dk = B.dk, a.dv = B.dv;
+    const double pairs = (double)n * l + (double)n * (n + 1) / 2;
+    TRY(launch(S, K_ATTN_BWD, 8.0 * H * pairs, (4.0 * n + 2.0 * r) * H * e + 16.0 * r * H,
+               [&] { return attn_bwd(dt, a, st); }));
+    TRY(launch(S, K_MISC, 0, 8.0 * n * H + 2 * nb, [&] {
+      return pack_dkv(dt, n, H, B.dk + (long)l * H, B.dv + (long)l * H,
+                      rowp(B.dqkv, l, 3 * H, e), st);
+    }));
+    // QKV backward: du = [dq dk dv] W_qkv
+    g = nn(n, H, 3 * H, rowp(B.dqkv, l, 3 * H, e), 3 * H, P.w_qkv);
+    g.C = S->sc.du, g.ldc = H;
+    TRY(run_gemm(S, K_GEMM_DX, g));
+    TRY(launch(S, K_MISC, 0, 3 * nb, [&] {
+      return colsum_acc(dt, n, 3 * H, rowp(B.dqkv, l, 3 * H, e), 3 * H, (float*)G.b_qkv, st);
+    }));
+    // LN1 backward + residual: dx = dx1 + LN1^T(du)
+    void* out = li == 0 ? dx : rowp(S->lb[li - 1].dy, l, H, e);
+    TRY(launch(S, K_NORM, 0, 4 * nb, [&] {
+      return ln_bwd(dt, n, H, S->sc.du, rowp(B.x_in, l, H, e), B.mean1 + l, B.rstd1 + l, P.ln1_g,
+                    rowp(B.dx1, l, H, e), out, st);
+    }));
+    TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
+      return ln_param_grads(dt, n, H, S->sc.du, rowp(B.x_in, l, H, e), B.mean1 + l, B.rstd1 + l,
+                            (float*)G.ln1_g, (float*)G.ln1_b, st);
+    }));
+    if (per_slice) {
+      tp_status s = wgrad_gemms(S, li, l, n);
+      if (s != TP_OK) return s;
+    }
+  }
+  if (!per_slice && l == 0 && !S->profiling) {
+    for (int li = NL - 1; li >= 0; --li) {
+      tp_status s = wgrad_gemms(S, li, 0, S->cached_len);
+      if (s != TP_OK) return s;
+    }
+  }
+  return TP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t tp_stage_workspace_bytes(const tp_stage_config* cfg) {
+  if (!config_ok(cfg)) return 0;
+  return carve(cfg, nullptr, nullptr, nullptr);
+}
+
+static bool layer_ptrs_ok(const tp_layer_ptrs& p) {
+  const void* a[] = {p.ln1_g, p.ln1_b, p.w_qkv, p.b_qkv, p.w_o,   p.b_o,
+                     p.ln2_g, p.ln2_b, p.w_fc1, p.b_fc1, p.w_fc2, p.b_fc2};
+  for (const void* v : a)
+    if (!v) return false;
+  return true;
+}
+
+tp_status tp_stage_init(const tp_stage_config* cfg, const tp_layer_ptrs* params,
+                        const tp_layer_ptrs* grads, void* workspace, size_t workspace_bytes,
+                        void* stream, tp_stage** out) {
+  if (!out) return TP_ERR_INVALID;
+  *out = nullptr;
+  if (!config_ok(cfg) || !params || !grads || !workspace) return TP_ERR_INVALID;
+  for (int i = 0; i < cfg->n_layers; ++i)
+    if (!layer_ptrs_ok(params[i]) || !layer_ptrs_ok(grads[i])) return TP_ERR_INVALID;
+  if (!config_supported(cfg)) return TP_ERR_UNSUPPORTED;
+  if (((uintptr_t)workspace & 255) || workspace_bytes < carve(cfg, nullptr, nullptr, nullptr))
+    return TP_ERR_WORKSPACE;
+  tp_stage* S = new (std::nothrow) tp_stage();
+  if (!S) return TP_ERR_INVALID;
+  S->cfg = *cfg;
+  S->H = cfg->hidden;
+  S->F = 4 * cfg->hidden;
+  S->heads = cfg->heads;
+  S->d = cfg->hidden / cfg->heads;
+  S->L = cfg->max_seq;
+  S->dt = cfg->dtype == TP_DTYPE_FP32 ? DT_FP32 : DT_BF16;
+  S->esz = cfg->dtype == TP_DTYPE_FP32 ? 4 : 2;
+  S->P.assign(params, params + cfg->n_layers);
+  S->G.assign(grads, grads + cfg->n_layers);
+  carve(cfg, workspace, &S->lb, &S->sc);
+  S->stream = (hipStream_t)stream;
+  *out = S;
+  return TP_OK;
+}
+
+void tp_stage_destroy(tp_stage* S) {
+  if (!S) return;
+  for (auto& p : S->pending) {
+    hipEventDestroy(p.a);
+    hipEventDestroy(p.b);
+  }
+  for (auto e : S->free_events) hipEventDestroy(e);
+  delete S;
+}
+
+tp_status tp_kv_prefix_reset(tp_stage* S) {
+  if (!S) return TP_ERR_INVALID;
+  const size_t n = (size_t)S->L * S->H;
+  for (auto& B : S->lb) {
+    TRY(fill_f32(B.dk, n, 0.f, S->stream));
+    TRY(fill_f32(B.dv, n, 0.f, S->stream));
+  }
+  S->cached_len = 0;
+  S->bwd_frontier = 0;
+  return TP_OK;
+}
+
+tp_status tp_slice_forward(tp_stage* S, int l, int r, const void* x, void* y) {
+  if (!S || !x || !y) return TP_ERR_INVALID;
+  if (l < 0 || r <= l || r > S->L) return TP_ERR_INVALID;
+  if (l != S->cached_len) return TP_ERR_ORDER;
+  tp_status s = forward_impl(S, l, r, x, y);
+  if (s != TP_OK) return s;
+  S->cached_len = r;
+  S->bwd_frontier = r;
+  return TP_OK;
+}
+
+tp_status tp_slice_backward(tp_stage* S, int l, int r, const void* dy, void* dx) {
+  if (!S || !dy || !dx) return TP_ERR_INVALID;
+  if (l < 0 || r <= l || r > S->L) return TP_ERR_INVALID;
+  if (r != S->bwd_frontier) return TP_ERR_ORDER;
+  tp_status s = backward_impl(S, l, r, dy, dx);
+  if (s != TP_OK) return s;
+  S->bwd_frontier = l;
+  return TP_OK;
+}
+
+tp_status tp_profile_slice_cost(tp_stage* S, const int* lens, int n_lens, const int* ctxs,
+                                int n_ctxs, int warmup, int reps, int64_t* t_fwd_ns,
+                                int64_t* t_bwd_ns) {
+  if (!S || !lens || !ctxs || !t_fwd_ns || !t_bwd_ns || n_lens < 1 || n_ctxs < 1 || warmup < 0 ||
+      reps < 1)
+    return TP_ERR_INVALID;
+  for (int i = 0; i < n_lens; ++i)
+    if (lens[i] < 1) return TP_ERR_INVALID;
+  for (int j = 0; j < n_ctxs; ++j)
+    if (ctxs[j] < 0) return TP_ERR_INVALID;
+  hipEvent_t e0, e1, e2;
+  if (hipEventCreate(&e0) != hipSuccess) return TP_ERR_HIP;
+  if (hipEventCreate(&e1) != hipSuccess) return TP_ERR_HIP;
+  if (hipEventCreate(&e2) != hipSuccess) return TP_ERR_HIP;
+  const bool was_timing = S->timing;
+  S->timing = false;
+  S->profiling = true;
+  tp_status status = TP_OK;
+  // deterministic, finite slice inputs
+  const size_t io = (size_t)S->L * S->H;
+  if (S->dt == DT_FP32) {
+    if (fill_f32((float*)S->sc.io_a, io, 0.5f, S->stream) != hipSuccess) status = TP_ERR_HIP;
+  } else {
+    if (fill_f32((float*)S->sc.io_a, io / 2, 0.5f, S->stream) != hipSuccess) status = TP_ERR_HIP;
+  }
+  std::vector<float> tf, tb;
+  for (int i = 0; i < n_lens && status == TP_OK; ++i)
+    for (int j = 0; j < n_ctxs && status == TP_OK; ++j) {
+      const int len = lens[i], ctx = ctxs[j];
+      const size_t idx = (size_t)i * n_ctxs + j;
+      if ((long)len + ctx > S->L) {
+        t_fwd_ns[idx] = t_bwd_ns[idx] = -1;
+        continue;
+      }
+      tf.clear();
+      tb.clear();
+      for (int rep = 0; rep < warmup + reps && status == TP_OK; ++rep) {
+        S->cached_len = ctx;
+        hipEventRecord(e0, S->stream);
+        status = forward_impl(S, ctx, ctx + len, S->sc.io_a, S->sc.io_b);
+        if (status != TP_OK) break;
+        hipEventRecord(e1, S->stream);
+        status = backward_impl(S, ctx, ctx + len, S->sc.io_a, S->sc.io_b);
+        if (status != TP_OK) break;
+        hipEventRecord(e2, S->stream);
+        if (hipEventSynchronize(e2) != hipSuccess) {
+          status = TP_ERR_HIP;
+          break;
+        }
+        float f = 0, b = 0;
+        hipEventElapsedTime(&f, e0, e1);
+        hipEventElapsedTime(&b, e1, e2);
+        if (rep >= warmup) {
+          tf.push_back(f);
+          tb.push_back(b);
+        }
+      }
+      if (status != TP_OK) break;
+      std::sort(tf.begin(), tf.end());
+      std::sort(tb.begin(), tb.end());
+      auto med = [](const std::vector<float>& v) {
+        const size_t m = v.size();
+        return m % 2 ? (double)v[m / 2] : 0.5 * ((double)v[m / 2 - 1] + v[m / 2]);
+      };
+      t_fwd_ns[idx] = (int64_t)std::llround(med(tf) * 1e6);
+      t_bwd_ns[idx] = (int64_t)std::llround(med(tb) * 1e6);
+    }
+  hipEventDestroy(e0);
+  hipEventDestroy(e1);
+  hipEventDestroy(e2);
+  S->profiling = false;
+  S->timing = was_timing;
+  S->cached_len = 0;
+  S->bwd_frontier = 0;
+  return status;
+}
+
+const char* tp_status_string(tp_status s) {
+  switch (s) {
+    case TP_OK: return "ok";
+    case TP_ERR_INVALID: return "invalid argument";
+    case TP_ERR_ORDER: return "slice out of order";
+    case TP_ERR_UNSUPPORTED: return "unsupported configuration";
+    case TP_ERR_WORKSPACE: return "workspace too small or misaligned";
+    case TP_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+tp_status tp_stage_enable_kernel_timing(tp_stage* S, int enable) {
+  if (!S) return TP_ERR_INVALID;
+  S->timing = enable != 0;
+  return TP_OK;
+}
+
+int tp_stage_kernel_stats(tp_stage* S, tp_kernel_stat* out, int cap) {
+  if (!S) return 0;
+  if (!S->pending.empty()) {
+    if (hipStreamSynchronize(S->stream) != hipSuccess) return 0;
+    for (auto& p : S->pending) {
+      float ms = 0.f;
+      hipEventElapsedTime(&ms, p.a, p.b);
+      S->launches[p.cls] += 1;
+      S->total_ms[p.cls] += ms;
+      S->flops[p.cls] += p.flops;
+      S->bytes[p.cls] += p.bytes;
+      S->free_events.push_back(p.a);
+      S->free_events.push_back(p.b);
+    }
+    S->pending.clear();
+  }
+  int w = 0;
+  for (int c = 0; c < K_N && out && w < cap; ++c) {
+    if (!S->launches[c]) continue;
+    std::memset(&out[w], 0, sizeof(tp_kernel_stat));
+    std::strncpy(out[w].name, kclass_name[c], sizeof(out[w].name) - 1);
+    out[w].launches = S->launches[c];
+    out[w].total_ms = S->total_ms[c];
+    out[w].flops = S->flops[c];
+    out[w].bytes = S->bytes[c];
+    ++w;
+  }
+  // reading resets the counters
+  for (int c = 0; c < K_N; ++c) {
+    S->launches[c] = 0;
+    S->total_ms[c] = S->flops[c] = S->bytes[c] = 0;
+  }
+  return w;
+}
+
+}  // extern "C"

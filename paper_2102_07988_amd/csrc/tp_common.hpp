@@ -1,0 +1,108 @@
+// Shared device/host helpers of the stage engine: storage types, bf16
+// rounding, wave/block reductions, launch-error plumbing.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/terapipe.h"
+
+namespace tp {
+
+// bf16 is carried as raw 16-bit storage; arithmetic is always fp32.
+struct bf16 {
+  uint16_t v;
+};
+
+__host__ __device__ inline float to_f32(float x) { return x; }
+__host__ __device__ inline float to_f32(bf16 x) {
+  union {
+    uint32_t u;
+    float f;
+  } c;
+  c.u = (uint32_t)x.v << 16;
+  return c.f;
+}
+
+// Round to nearest, ties to even (the rounding the stage uses for every bf16
+// store); NaN stays NaN.
+__host__ __device__ inline uint16_t f32_to_bf16_bits(float f) {
+  union {
+    uint32_t u;
+    float f;
+  } c;
+  c.f = f;
+  uint32_t u = c.u;
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <typename T>
+__host__ __device__ inline T from_f32(float x);
+template <>
+__host__ __device__ inline float from_f32<float>(float x) {
+  return x;
+}
+template <>
+__host__ __device__ inline bf16 from_f32<bf16>(float x) {
+  bf16 b;
+  b.v = f32_to_bf16_bits(x);
+  return b;
+}
+
+template <typename T>
+__device__ inline float ld(const T* p) {
+  return to_f32(*p);
+}
+template <typename T>
+__device__ inline void st(T* p, float v) {
+  *p = from_f32<T>(v);
+}
+
+// GELU, tanh form: 0.5 z (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3))).
+__device__ inline float gelu_tanh(float z) {
+  const float c = 0.7978845608028654f, a = 0.044715f;
+  return 0.5f * z * (1.0f + tanhf(c * (z + a * z * z * z)));
+}
+__device__ inline float gelu_tanh_grad(float z) {
+  const float c = 0.7978845608028654f, a = 0.044715f;
+  const float th = tanhf(c * (z + a * z * z * z));
+  return 0.5f * (1.0f + th) + 0.5f * z * (1.0f - th * th) * c * (1.0f + 3.0f * a * z * z);
+}
+
+__device__ inline float wave_sum(float v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ inline float wave_max(float v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Block-wide sum for blockDim.x a multiple of 64 (<= 1024).  `red` is LDS of
+// >= 16 floats.  Every thread gets the result.
+__device__ inline float block_sum(float v, float* red) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  v = wave_sum(v);
+  __syncthreads();
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  float s = 0.f;
+  for (int i = 0; i < nw; ++i) s += red[i];
+  return s;
+}
+__device__ inline float block_max(float v, float* red) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  v = wave_max(v);
+  __syncthreads();
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  float s = -INFINITY;
+  for (int i = 0; i < nw; ++i) s = fmaxf(s, red[i]);
+  return s;
+}
+
+inline int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
+
+}  // namespace tp

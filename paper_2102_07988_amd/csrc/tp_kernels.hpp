@@ -1,0 +1,88 @@
+// Launchers of the stage's device kernels.  All pointers are device pointers;
+// element types follow the stage dtype (0 = bf16, 1 = fp32) unless the name or
+// the comment says fp32.  Every launcher enqueues on `s` and returns the launch
+// status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tp {
+
+enum Dtype { DT_BF16 = 0, DT_FP32 = 1 };
+
+// GEMM epilogues (what happens to acc = sum_k A(m,k) B(k,n), fp32):
+enum EpiKind {
+  EPI_STORE = 0,  // C[m][n] = acc (+ bias[n])
+  EPI_QKV = 1,    // v = acc + bias[n]; n < H -> q[m][n], n < 2H -> k[m][n-H], else v[m][n-2H]
+  EPI_RESID = 2,  // C[m][n] = acc + bias[n] + R[m][n]
+  EPI_GELU = 3,   // z = acc + bias[n]; C[m][n] = z; C2[m][n] = GELU(z)
+  EPI_DGELU = 4,  // C[m][n] = acc * GELU'(R[m][n])
+  EPI_ACC_F32 = 5 // Cf[m][n] += acc (fp32 output, read-modify-write)
+};
+
+struct GemmArgs {
+  int M = 0, N = 0, K = 0;
+  const void* A = nullptr;  // A(m,k) = A[m*sam + k*sak]
+  long sam = 0, sak = 0;
+  const void* B = nullptr;  // B(k,n) = B[k*sbk + n*sbn]
+  long sbk = 0, sbn = 0;
+  int epi = EPI_STORE;
+  const void* bias = nullptr;  // [N], stage dtype; may be null
+  void* C = nullptr;           // rows of ldc elements (stage dtype; fp32 for EPI_ACC_F32)
+  long ldc = 0;
+  const void* R = nullptr;  // residual (EPI_RESID) or pre-activation z (EPI_DGELU)
+  long ldr = 0;
+  void* C2 = nullptr;  // GELU output (EPI_GELU)
+  long ldc2 = 0;
+  void *q = nullptr, *k = nullptr, *v = nullptr;  // EPI_QKV destinations, row stride H
+  int H = 0;
+};
+
+hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s);
+// Generic (any strides, any dtype) tiled FMA GEMM; the bf16 fast path falls back
+// to it for shapes it does not cover.
+hipError_t gemm_generic(int dtype, const GemmArgs& a, hipStream_t s);
+
+// Prefix-causal attention over a slice: queries t in [l, r), keys s in [0, t].
+// q, o: rows [r-l][H] (row i = token l+i); kc, vc: cache rows [Lmax][H] from
+// token 0; lse: fp32 [heads][Lmax] (absolute token index).
+struct AttnArgs {
+  int l = 0, r = 0, H = 0, heads = 0, d = 0, Lmax = 0;
+  float scale = 1.f;
+  const void* q = nullptr;
+  const void* kc = nullptr;
+  const void* vc = nullptr;
+  void* o = nullptr;
+  float* lse = nullptr;
+  // backward
+  const void* dout = nullptr;  // [r-l][H]
+  float* D = nullptr;          // fp32 [heads][Lmax] scratch: rowsum(dO * O)
+  void* dq = nullptr;          // rows of ld_dq elements (row i = token l+i)
+  long ld_dq = 0;
+  float* dk = nullptr;  // fp32 [Lmax][H] accumulation buffers (absolute rows)
+  float* dv = nullptr;
+};
+hipError_t attn_fwd(int dtype, const AttnArgs& a, hipStream_t s);
+hipError_t attn_bwd(int dtype, const AttnArgs& a, hipStream_t s);
+
+// LayerNorm over rows of H: u = g * (x - mean) * rstd + b.  If x_copy is not
+// null, the input rows are also copied there.
+hipError_t ln_fwd(int dtype, int n, int H, const void* x, void* x_copy, const void* g,
+                  const void* b, void* u, float* mean, float* rstd, float eps, hipStream_t s);
+// dx = LN^T(du) + resid (resid may be null).
+hipError_t ln_bwd(int dtype, int n, int H, const void* du, const void* x, const float* mean,
+                  const float* rstd, const void* g, const void* resid, void* dx, hipStream_t s);
+// dg[i] += sum_t du[t][i] * xhat[t][i];  db[i] += sum_t du[t][i]   (fp32 outputs)
+hipError_t ln_param_grads(int dtype, int n, int H, const void* du, const void* x,
+                          const float* mean, const float* rstd, float* dg, float* db,
+                          hipStream_t s);
+// out[j] += sum_{i<n} A[i*lda + j], j < N (fp32 output)
+hipError_t colsum_acc(int dtype, int n, int N, const void* A, long lda, float* out, hipStream_t s);
+// dqkv[i][H + j] = dk[l+i][j], dqkv[i][2H + j] = dv[l+i][j] (stage dtype <- fp32)
+hipError_t pack_dkv(int dtype, int n, int H, const float* dk, const float* dv, void* dqkv,
+                    hipStream_t s);
+hipError_t fill_f32(float* p, size_t n, float v, hipStream_t s);
+hipError_t copy_rows(int dtype, int n, int H, const void* src, void* dst, hipStream_t s);
+
+}  // namespace tp

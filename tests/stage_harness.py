@@ -1,0 +1,59 @@
+"""Shared helpers of the GPU parity tests: build the same seeded stage for the
+HIP path (through the C ABI) and for the oracle, run a sequence, compare."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from paper_2102_07988_amd import synth
+
+PARAM_KEYS = synth.PARAM_NAMES
+
+
+def rel_l2(a, b) -> float:
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    nb = np.linalg.norm(b)
+    d = np.linalg.norm(a - b)
+    return float(d / nb) if nb > 0 else float(d)
+
+
+def make_inputs(n_layers, H, L, dtype, seeds=(0, 1, 2), randomize_ln=False):
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    sx, sp, sdy = seeds
+    params = synth.stage_params(n_layers, H, seed=sp, dtype=tdt, randomize_ln=randomize_ln)
+    x = synth.hidden_states(L, H, seed=sx, dtype=tdt)
+    dy = synth.upstream_grad(L, H, seed=sdy, dtype=tdt)
+    return params, x, dy
+
+
+def run_gpu(params, x, dy, H, heads, L, dtype, fwd_lens, bwd_lens=None, wgrad="per_slice",
+            device="cuda:0"):
+    from paper_2102_07988_amd import terapipe as tp
+    dparams = [{k: v.to(device).contiguous() for k, v in p.items()} for p in params]
+    st = tp.Stage(dparams, H, heads, L, dtype=dtype, wgrad=wgrad)
+    y, dx = st.run_sequence(x.to(device), dy.to(device), fwd_lens, bwd_lens)
+    torch.cuda.synchronize()
+    out = {"y": y.float().cpu().numpy(), "dx": dx.float().cpu().numpy(),
+           "grads": [{k: v.cpu().numpy() for k, v in g.items()} for g in st.grads]}
+    del st
+    return out
+
+
+def run_oracle(params, x, dy, H, heads, L, fwd_lens, bwd_lens=None):
+    from oracle import OracleStage
+    ost = OracleStage(synth.params_f64(params), H, heads, L)
+    y, dx = ost.run_sequence(synth.to_f64(x), synth.to_f64(dy), fwd_lens, bwd_lens)
+    return {"y": y, "dx": dx, "grads": ost.grads}
+
+
+def compare(got, ref, tol, label=""):
+    errs = {"y": rel_l2(got["y"], ref["y"]), "dx": rel_l2(got["dx"], ref["dx"])}
+    for li, (g, r) in enumerate(zip(got["grads"], ref["grads"])):
+        for k in PARAM_KEYS:
+            errs[f"L{li}.{k}"] = rel_l2(g[k], r[k])
+    worst = max(errs, key=errs.get)
+    print(f"[{label}] worst rel-L2 {worst} = {errs[worst]:.3e}", flush=True)
+    bad = {k: v for k, v in errs.items() if not (v <= tol)}
+    assert not bad, f"{label}: rel-L2 above {tol}: {bad}"
+    return errs

@@ -1,0 +1,89 @@
+"""GPU parity: the HIP stage through the C ABI against the fp64 oracle on the
+same seeded inputs.  Tolerances (rel-L2 per tensor: y, dx and every parameter
+gradient): 1e-4 in the fp32 validation mode, 2e-2 in bf16."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2102_07988_amd import synth
+from stage_harness import compare, make_inputs, rel_l2, run_gpu, run_oracle
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"fp32": 1e-4, "bf16": 2e-2}
+
+
+def _case(n_layers, H, heads, L, dtype, fwd, bwd=None, wgrad="per_slice", seeds=(0, 1, 2),
+          randomize_ln=False, label=""):
+    print(f"case {label}: layers={n_layers} H={H} heads={heads} L={L} {dtype} {wgrad} "
+          f"fwd={fwd} bwd={bwd}", flush=True)
+    params, x, dy = make_inputs(n_layers, H, L, dtype, seeds, randomize_ln)
+    got = run_gpu(params, x, dy, H, heads, L, dtype, fwd, bwd, wgrad)
+    ref = run_oracle(params, x, dy, H, heads, L, fwd, bwd)
+    return compare(got, ref, TOL[dtype], label)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_tiny_config(dtype):
+    """1 layer, hidden 64, 4 heads, seq 32, slicing [8, 8, 16], seed 0."""
+    _case(1, 64, 4, 32, dtype, [8, 8, 16], seeds=(0, 0, 0), randomize_ln=True, label="tiny")
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("wgrad", ["per_slice", "deferred"])
+def test_two_layers_ragged_slicings(dtype, wgrad):
+    """2 layers, ragged forward slicing, different backward slicing, tails not
+    multiples of any tile."""
+    _case(2, 128, 4, 100, dtype, [37, 1, 29, 33], [50, 7, 43], wgrad, seeds=(3, 4, 5),
+          randomize_ln=True, label="ragged")
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_head_widths(dtype):
+    for H, heads in [(64, 4), (128, 4), (256, 4), (512, 4)]:  # d = 16, 32, 64, 128
+        _case(1, H, heads, 48, dtype, [16, 32], label=f"d={H // heads}")
+
+
+def test_gpt3_13b_shape_reduced_sequence():
+    """hidden 5120, 40 heads (d = 128), bf16, two slices of 16 after nothing cached."""
+    _case(1, 5120, 40, 32, "bf16", [16, 16], label="13B-shape")
+
+
+def test_gpt3_1p3b_shape_two_layers():
+    """GPT-3 1.3B-shaped stage (2 layers, hidden 2048, 16 heads) on a 512-token
+    sequence cut into 2 x 256 (the slice shape of the 8 x 256 workload)."""
+    _case(2, 2048, 16, 512, "bf16", [256, 256], label="1.3B-shape")
+
+
+def test_gpu_slicing_invariance_fp32():
+    """Different slicings of one sequence give the same result on the GPU."""
+    H, heads, L = 128, 4, 96
+    params, x, dy = make_inputs(2, H, L, "fp32", (7, 8, 9))
+    base = run_gpu(params, x, dy, H, heads, L, "fp32", [96])
+    for fwd, bwd in [([32, 32, 32], None), ([1] * 96, [48, 48]), ([95, 1], [1, 95])]:
+        got = run_gpu(params, x, dy, H, heads, L, "fp32", fwd, bwd)
+        assert rel_l2(got["y"], base["y"]) < 1e-5
+        assert rel_l2(got["dx"], base["dx"]) < 1e-5
+        for g, b in zip(got["grads"], base["grads"]):
+            for k in g:
+                assert rel_l2(g[k], b[k]) < 1e-5, k
+
+
+def test_order_errors_leave_state():
+    from paper_2102_07988_amd import terapipe as tp
+    H, heads, L = 64, 4, 32
+    params, x, dy = make_inputs(1, H, L, "fp32", (0, 0, 0))
+    dparams = [{k: v.cuda() for k, v in p.items()} for p in params]
+    st = tp.Stage(dparams, H, heads, L, dtype="fp32")
+    st.reset()
+    xd = x.cuda()
+    st.forward(0, 8, xd[:8])
+    with pytest.raises(tp.TerapipeError) as e:
+        st.forward(4, 12, xd[4:12])
+    assert e.value.status == tp.TP_ERR_ORDER
+    st.forward(8, 16, xd[8:16])  # still accepted: the failed call changed nothing
+    with pytest.raises(tp.TerapipeError):
+        st.backward(0, 8, xd[:8])  # frontier is 16
+    st.backward(8, 16, xd[8:16])
+    st.backward(0, 8, xd[:8])
+    torch.cuda.synchronize()
