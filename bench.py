@@ -1,0 +1,185 @@
+"""Benchmark of one TeraPipe pipeline stage on one MI355X.
+
+A step is one training sequence through the stage: reset the K/V prefix, run
+the forward of every token slice in order, then the backward of every slice in
+reverse (the weight-gradient GEMMs included: per slice, or once at the end of
+the sequence in the deferred mode).  Throughput is algorithmic flops per
+second: per layer and slice, 24 n H^2 (projections) + 4 H per causal
+(query, key <= query) pair forward, backward twice forward.
+
+Prints one JSON line.  Per-kernel-class times are measured with HIP events on
+the stage's stream over the timed region; `roofline` reports the class with
+the largest total time.  `cpu_baseline` times the fp64 CPU oracle on a bounded
+sample of the same workload (one layer, a short slice).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+# name: (layers, hidden, heads, seq, default slicing)
+WORKLOADS = {
+    "gpt3-175b-stage": (2, 12288, 96, 2048, [256] * 8),
+    "gpt3-175b-stage-8k": (2, 12288, 96, 8192, [512] * 16),
+    "gpt3-13b-stage": (2, 5120, 40, 2048, [256] * 8),
+    "gpt3-1.3b-stage": (2, 2048, 16, 2048, [256] * 8),
+}
+
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def parse_slicing(s: str, L: int, default):
+    if not s:
+        return list(default)
+    if s.startswith("uniform"):
+        n = int(s[len("uniform"):])
+        assert L % n == 0
+        return [n] * (L // n)
+    lens = [int(v) for v in s.split(",")]
+    assert sum(lens) == L, "slicing must sum to the sequence length"
+    return lens
+
+
+def cpu_baseline(params0, x, dy, hidden: int, heads: int, n_tokens: int):
+    """Time the fp64 oracle (all host threads) on one layer of the workload
+    (the benchmark's own layer-0 parameters) over one slice of the first
+    n_tokens tokens after no context: forward + backward."""
+    import numpy as np
+    import torch
+
+    from oracle import OracleStage, slice_flops
+
+    p64 = {k: v.detach().to("cpu").to(torch.float64).numpy() for k, v in params0.items()}
+    x64 = x[:n_tokens].to("cpu").to(torch.float64).numpy()
+    dy64 = dy[:n_tokens].to("cpu").to(torch.float64).numpy()
+    st = OracleStage([p64], hidden, heads, n_tokens)
+    del p64
+    t0 = time.perf_counter()
+    st.run_sequence(x64, dy64, [n_tokens])
+    dt = time.perf_counter() - t0
+    flops = slice_flops(n_tokens, 0, hidden)
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "seconds": round(dt, 3),
+            "sample": f"1 layer of the same shape (H={hidden}, {heads} heads), one slice of "
+                      f"{n_tokens} tokens at context 0, forward+backward, fp64"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="gpt3-175b-stage", choices=sorted(WORKLOADS))
+    ap.add_argument("--slicing", default="", help="'uniform256' or comma-separated lengths")
+    ap.add_argument("--wgrad", default="deferred", choices=["deferred", "per_slice"])
+    ap.add_argument("--cpu-baseline-tokens", type=int, default=48)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-timing", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs one pipeline stage on one GPU; "
+                                   "--gpus above 1 is not supported", "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+
+    from paper_2102_07988_amd import synth
+    from paper_2102_07988_amd import terapipe as tp
+
+    n_layers, H, heads, L, default_sl = WORKLOADS[args.workload]
+    lens = parse_slicing(args.slicing, L, default_sl)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    bf = torch.bfloat16
+    params = synth.stage_params(n_layers, H, seed=synth.SEED_PARAMS, dtype=bf, device=dev)
+    x = synth.hidden_states(L, H, seed=synth.SEED_X, dtype=bf, device=dev)
+    dy = synth.upstream_grad(L, H, seed=synth.SEED_DY, dtype=bf, device=dev)
+    st = tp.Stage(params, H, heads, L, dtype="bf16", wgrad=args.wgrad)
+    y = torch.empty_like(x)
+    dx = torch.empty_like(dy)
+    bounds = [0]
+    for n in lens:
+        bounds.append(bounds[-1] + n)
+
+    def step():
+        st.reset()
+        for i in range(len(lens)):
+            l, r = bounds[i], bounds[i + 1]
+            st.forward(l, r, x[l:r], out=y[l:r])
+        for i in range(len(lens) - 1, -1, -1):
+            l, r = bounds[i], bounds[i + 1]
+            st.backward(l, r, dy[l:r], out=dx[l:r])
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if not args.no_kernel_timing:
+        st.enable_kernel_timing(True)
+        st.kernel_stats()  # clears the counters
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    stats = st.kernel_stats() if not args.no_kernel_timing else {}
+    st.enable_kernel_timing(False)
+
+    flops_step = 0
+    c = 0
+    for n in lens:
+        flops_step += tp.slice_flops(n, c, H) * n_layers
+        c += n
+    ms = (t1 - t0) * 1e3 / args.steps
+    value = flops_step / (ms * 1e-3) / 1e12
+    finite = bool(torch.isfinite(y.float()).all() and torch.isfinite(dx.float()).all())
+
+    roofline = None
+    kernels = {}
+    if stats:
+        for name, s in stats.items():
+            kernels[name] = {"launches": s["launches"], "ms_per_step": s["total_ms"] / args.steps,
+                             "avg_us": 1e3 * s["total_ms"] / max(1, s["launches"])}
+        dom = max(stats, key=lambda k: stats[k]["total_ms"])
+        s = stats[dom]
+        secs = s["total_ms"] * 1e-3
+        if dom.startswith("gemm"):
+            ach = s["flops"] / secs / 1e12
+            roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2),
+                        "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                        "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None}
+        else:
+            ach = s["bytes"] / secs / 1e9
+            roofline = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1),
+                        "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None}
+
+    out = {
+        "metric": "slice fwd+bwd TFLOP/s (whole sequence through one pipeline stage)",
+        "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": args.workload, "layers": n_layers, "hidden": H, "heads": heads,
+                   "seq_len": L, "batch": 1, "slicing": lens, "wgrad": args.wgrad,
+                   "global_batch": 1, "parallelism": "one pipeline stage"},
+        "pct_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
+        "flops_per_step": flops_step, "outputs_finite": finite,
+        "roofline": roofline, "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(params[0], x, dy, H, heads, args.cpu_baseline_tokens)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
