@@ -66,7 +66,7 @@ typedef enum { TP_WGRAD_PER_SLICE = 0, TP_WGRAD_DEFERRED = 1 } tp_wgrad_mode;
 typedef struct {
   int n_layers;   /* layers in this stage, >= 1 */
   int hidden;     /* H; FFN width is 4H */
-  int heads;      /* a; head width d = H / a must be 16, 32, 64 or 128 */
+  int heads;      /* a; head width d = H / a must be 16, 32, 64 or 128; H % 8 == 0, H <= 16384 */
   int max_seq;    /* largest sequence length L the stage will see */
   int dtype;      /* tp_dtype */
   int wgrad_mode; /* tp_wgrad_mode */
@@ -114,7 +114,8 @@ tp_status tp_kv_prefix_reset(tp_stage *stage);
  * device).  Requires 0 <= l < r <= max_seq (else TP_ERR_INVALID) and l equal to
  * the number of cached tokens (else TP_ERR_ORDER).  Appends the slice's keys
  * and values to each layer's cache, saves what backward needs, and sets the
- * cached length and the backward frontier to r.  x and y must not overlap. */
+ * cached length and the backward frontier to r.  x and y must not overlap and
+ * must be 16-byte aligned (else TP_ERR_INVALID). */
 tp_status tp_slice_forward(tp_stage *stage, int l, int r, const void *x, void *y);
 
 /* Backward of token slice [l, r) through every layer, in reverse layer order.
@@ -125,7 +126,7 @@ tp_status tp_slice_forward(tp_stage *stage, int l, int r, const void *x, void *y
  * this slice's contributions to the parameter gradients; the gradient that
  * queries in [l, r) send to earlier keys/values is added to the dK/dV buffer.
  * Sets the frontier to l; in DEFERRED mode the weight-gradient GEMMs run when
- * l reaches 0.  dy and dx must not overlap. */
+ * l reaches 0.  dy and dx must not overlap and must be 16-byte aligned. */
 tp_status tp_slice_backward(tp_stage *stage, int l, int r, const void *dy, void *dx);
 
 /* Measure the per-slice costs t_fwd(len, ctx) and t_bwd(len, ctx) of Eq. 4 on

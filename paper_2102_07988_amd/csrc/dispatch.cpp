@@ -8,20 +8,34 @@ hipError_t attn_fwd_generic(int dtype, const AttnArgs& a, hipStream_t s);
 hipError_t attn_bwd_generic(int dtype, const AttnArgs& a, hipStream_t s);
 
 hipError_t gemm_mfma_bf16(const GemmArgs& a, hipStream_t s);
+hipError_t gemm_dma_bf16(const GemmArgs& a, hipStream_t s);
 
 hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s) {
   if (dtype == DT_BF16) {
-    const hipError_t e = gemm_mfma_bf16(a, s);
+    hipError_t e = gemm_dma_bf16(a, s);
+    if (e != hipErrorNotSupported) return e;
+    e = gemm_mfma_bf16(a, s);
     if (e != hipErrorNotSupported) return e;
   }
   return gemm_generic(dtype, a, s);
 }
 
+hipError_t attn_fwd_mfma_bf16(const AttnArgs& a, hipStream_t s);
+hipError_t attn_bwd_mfma_bf16(const AttnArgs& a, hipStream_t s);
+
 hipError_t attn_fwd(int dtype, const AttnArgs& a, hipStream_t s) {
+  if (dtype == DT_BF16) {
+    const hipError_t e = attn_fwd_mfma_bf16(a, s);
+    if (e != hipErrorNotSupported) return e;
+  }
   return attn_fwd_generic(dtype, a, s);
 }
 
 hipError_t attn_bwd(int dtype, const AttnArgs& a, hipStream_t s) {
+  if (dtype == DT_BF16) {
+    const hipError_t e = attn_bwd_mfma_bf16(a, s);
+    if (e != hipErrorNotSupported) return e;
+  }
   return attn_bwd_generic(dtype, a, s);
 }
 

@@ -2,11 +2,10 @@
 // accumulation in v_mfma_f32_32x32x16_bf16, followed by the stage's fused
 // epilogues.
 //
-// Block tile BM x BN x 64 with four waves in a 2 x 2 arrangement; each wave
-// owns a (BM/2) x (BN/2) sub-tile made of 32 x 32 MFMA tiles.  Both operands
-// sit in LDS k-contiguous ([row][64 k + 8 pad], the pad keeps the 16-byte
-// fragment reads of 16 consecutive rows on distinct banks), so one ds_read_b128
-// gives a lane its 8 consecutive k values.  An operand whose global layout is
+// Block tile BM x BN x 64 with WGM x WGN waves; each wave owns a
+// (BM/WGM) x (BN/WGN) sub-tile made of 32 x 32 MFMA tiles.  Both operands sit
+// in LDS k-contiguous (64 k per row, 16-byte chunks XOR-swizzled by row), so
+// one ds_read_b128 gives a lane its 8 consecutive k values.  An operand whose global layout is
 // k-contiguous (activations; weights [out][in] in the forward) is copied with
 // 16-byte loads; an operand that is contiguous along m or n (weights in the
 // dX products, token-major activations and gradients in the dW products) is
@@ -16,6 +15,8 @@
 #include "tp_common.hpp"
 #include "tp_kernels.hpp"
 
+#include <algorithm>
+
 namespace tp {
 
 namespace {
@@ -24,8 +25,14 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int BK = 64;
-constexpr int LDK = BK + 8;  // LDS row stride in bf16 elements
-constexpr int NT = 256;
+
+// LDS tile layout: row r holds 64 k values (128 bytes, no padding); its eight
+// 16-byte chunks are permuted by chunk ^ swz(r).  With swz(r) = (r ^ r/8) & 7
+// the fragment reads of 16 consecutive rows at one chunk hit 16 distinct
+// 16-byte bank groups, and the transposed 8-byte writes of one instruction
+// spread over all chunks.
+__device__ inline int swz(int r) { return (r ^ (r >> 3)) & 7; }
+__device__ inline int lds_off(int r, int k) { return r * BK + ((((k >> 3) ^ swz(r))) << 3) + (k & 7); }
 
 template <typename T, int EPI>
 __device__ inline void epi_store(const GemmArgs& a, int m, int n, float acc) {
@@ -56,17 +63,22 @@ __device__ inline void epi_store(const GemmArgs& a, int m, int n, float acc) {
   }
 }
 
+__device__ inline uint4 pack8(const uint16_t* t) {
+  return make_uint4(t[0] | (uint32_t)t[1] << 16, t[2] | (uint32_t)t[3] << 16,
+                    t[4] | (uint32_t)t[5] << 16, t[6] | (uint32_t)t[7] << 16);
+}
+
 // Operand tile of R rows (m or n) by BK k values, k-contiguous in global
 // memory: X(r, k) = X[r * ld + k].  Chunks of 8 k values (16 bytes).
-template <int R>
+template <int R, int NTH>
 struct TileKC {
-  static constexpr int CH = R * (BK / 8) / NT;  // chunks per thread
+  static constexpr int CH = R * (BK / 8) / NTH;  // chunks per thread
   static_assert(CH >= 1, "tile too small");
   uint4 v[CH];
   __device__ void load(const uint16_t* X, long ld, int r0, int rmax, int k0, int kmax) {
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
-      const int c = threadIdx.x + NT * i;
+      const int c = threadIdx.x + NTH * i;
       const int r = c >> 3, kc = (c & 7) * 8;
       const int gr = r0 + r, gk = k0 + kc;
       if (gr < rmax && gk + 8 <= kmax) {
@@ -76,106 +88,101 @@ struct TileKC {
 #pragma unroll
         for (int e = 0; e < 8; ++e)
           t[e] = (gr < rmax && gk + e < kmax) ? X[(long)gr * ld + gk + e] : (uint16_t)0;
-        v[i] = make_uint4(t[0] | (uint32_t)t[1] << 16, t[2] | (uint32_t)t[3] << 16,
-                          t[4] | (uint32_t)t[5] << 16, t[6] | (uint32_t)t[7] << 16);
+        v[i] = pack8(t);
       }
     }
   }
   __device__ void store(uint16_t* lds) const {
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
-      const int c = threadIdx.x + NT * i;
+      const int c = threadIdx.x + NTH * i;
       const int r = c >> 3, kc = (c & 7) * 8;
-      *(uint4*)(lds + r * LDK + kc) = v[i];
+      *(uint4*)(lds + lds_off(r, kc)) = v[i];
     }
   }
 };
 
 // Operand tile of R rows (m or n) by BK k values, contiguous along r in global
 // memory: X(r, k) = X[k * ld + r].  Blocks of 4 k x 8 r, transposed in registers.
-template <int R>
+template <int R, int NTH>
 struct TileMC {
-  static constexpr int NB = (BK / 4) * (R / 8);        // blocks per tile
-  static constexpr int PER = (NB + NT - 1) / NT;       // blocks per thread
-  uint2 v[PER][4];  // [block][k row] : 8 r values of one k (16 bytes as 2 x uint2)
-  uint2 w[PER][4];
+  static constexpr int NB = (BK / 4) * (R / 8);   // blocks per tile
+  static constexpr int PER = (NB + NTH - 1) / NTH;  // blocks per thread
+  uint4 x[PER][4];  // [block][k row]: 8 r values of one k
   __device__ void load(const uint16_t* X, long ld, int r0, int rmax, int k0, int kmax) {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int b = threadIdx.x + NT * i;
-      if (b >= NB) break;
+      const int b = threadIdx.x + NTH * i;
+      if (NB % NTH != 0 && b >= NB) break;
       const int kb = b / (R / 8), rb = b % (R / 8);
       const int gr = r0 + rb * 8;
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
         const int gk = k0 + kb * 4 + kk;
-        uint4 x;
         if (gk < kmax && gr + 8 <= rmax) {
-          x = *(const uint4*)(X + (long)gk * ld + gr);
+          x[i][kk] = *(const uint4*)(X + (long)gk * ld + gr);
         } else {
           uint16_t t[8];
 #pragma unroll
           for (int e = 0; e < 8; ++e)
             t[e] = (gk < kmax && gr + e < rmax) ? X[(long)gk * ld + gr + e] : (uint16_t)0;
-          x = make_uint4(t[0] | (uint32_t)t[1] << 16, t[2] | (uint32_t)t[3] << 16,
-                         t[4] | (uint32_t)t[5] << 16, t[6] | (uint32_t)t[7] << 16);
+          x[i][kk] = pack8(t);
         }
-        v[i][kk] = make_uint2(x.x, x.y);
-        w[i][kk] = make_uint2(x.z, x.w);
       }
     }
   }
-  // element e (0..7) of k row kk
-  __device__ static uint32_t half_word(const uint2& lo, const uint2& hi, int e) {
-    const uint32_t d = e < 2 ? lo.x : e < 4 ? lo.y : e < 6 ? hi.x : hi.y;
-    return d;
+  __device__ static uint32_t word(const uint4& v, int w) {
+    return w == 0 ? v.x : w == 1 ? v.y : w == 2 ? v.z : v.w;
   }
   __device__ void store(uint16_t* lds) const {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int b = threadIdx.x + NT * i;
-      if (b >= NB) break;
+      const int b = threadIdx.x + NTH * i;
+      if (NB % NTH != 0 && b >= NB) break;
       const int kb = b / (R / 8), rb = b % (R / 8);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        // output row r = rb*8 + e holds k = kb*4 + 0..3
-        const uint32_t d0 = half_word(v[i][0], w[i][0], e), d1 = half_word(v[i][1], w[i][1], e);
-        const uint32_t d2 = half_word(v[i][2], w[i][2], e), d3 = half_word(v[i][3], w[i][3], e);
+        // LDS row rb*8 + e receives k = kb*4 .. kb*4+3
         const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
-        const uint32_t p0 = __builtin_amdgcn_perm(d1, d0, sel);
-        const uint32_t p1 = __builtin_amdgcn_perm(d3, d2, sel);
-        *(uint2*)(lds + (rb * 8 + e) * LDK + kb * 4) = make_uint2(p0, p1);
+        const uint32_t p0 = __builtin_amdgcn_perm(word(x[i][1], e >> 1), word(x[i][0], e >> 1), sel);
+        const uint32_t p1 = __builtin_amdgcn_perm(word(x[i][3], e >> 1), word(x[i][2], e >> 1), sel);
+        *(uint2*)(lds + lds_off(rb * 8 + e, kb * 4)) = make_uint2(p0, p1);
       }
     }
   }
 };
 
-template <int R, bool KC>
+template <int R, int NTH, bool KC>
 struct TileSel;
-template <int R>
-struct TileSel<R, true> {
-  using type = TileKC<R>;
+template <int R, int NTH>
+struct TileSel<R, NTH, true> {
+  using type = TileKC<R, NTH>;
 };
-template <int R>
-struct TileSel<R, false> {
-  using type = TileMC<R>;
+template <int R, int NTH>
+struct TileSel<R, NTH, false> {
+  using type = TileMC<R, NTH>;
 };
 
-template <int BM, int BN, bool A_KC, bool B_KC, int EPI>
-__global__ __launch_bounds__(NT) void gemm_mfma_kernel(GemmArgs a) {
-  constexpr int WM = BM / 2, WN = BN / 2, FM = WM / 32, FN = WN / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t As[BM * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[BN * LDK];
+template <int BM, int BN, int WGM, int WGN, bool A_KC, bool B_KC, int EPI, bool SPLIT>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_mfma_kernel(GemmArgs a) {
+  constexpr int NTH = 64 * WGM * WGN;
+  constexpr int WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
+  static_assert(FM >= 1 && FN >= 1, "wave tile below 32 x 32");
+  __shared__ __attribute__((aligned(16))) uint16_t As[BM * BK];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[BN * BK];
   const uint16_t* A = (const uint16_t*)a.A;
   const uint16_t* B = (const uint16_t*)a.B;
   const long lda = A_KC ? a.sam : a.sak;
   const long ldb = B_KC ? a.sbn : a.sbk;
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm0 = (wave >> 1) * WM, wn0 = (wave & 1) * WN;
+  const int wm0 = (wave / WGN) * WM, wn0 = (wave % WGN) * WN;
+  // reduction range of this split
+  const int kbeg = SPLIT ? blockIdx.z * a.k_split : 0;
+  const int kend = SPLIT ? min(a.K, kbeg + a.k_split) : a.K;
 
-  typename TileSel<BM, A_KC>::type ta;
-  typename TileSel<BN, B_KC>::type tb;
+  typename TileSel<BM, NTH, A_KC>::type ta;
+  typename TileSel<BN, NTH, B_KC>::type tb;
   f32x16_t acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
@@ -184,31 +191,31 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(GemmArgs a) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  const int nk = (a.K + BK - 1) / BK;
-  ta.load(A, lda, m0, a.M, 0, a.K);
-  tb.load(B, ldb, n0, a.N, 0, a.K);
-  ta.store(As);
-  tb.store(Bs);
+  const int nk = (kend - kbeg + BK - 1) / BK;
+  if (nk > 0) {
+    ta.load(A, lda, m0, a.M, kbeg, kend);
+    tb.load(B, ldb, n0, a.N, kbeg, kend);
+    ta.store(As);
+    tb.store(Bs);
+  }
   __syncthreads();
   const int fr = lane & 31, fk = (lane >> 5) * 8;
   for (int kt = 0; kt < nk; ++kt) {
     if (kt + 1 < nk) {
-      ta.load(A, lda, m0, a.M, (kt + 1) * BK, a.K);
-      tb.load(B, ldb, n0, a.N, (kt + 1) * BK, a.K);
+      ta.load(A, lda, m0, a.M, kbeg + (kt + 1) * BK, kend);
+      tb.load(B, ldb, n0, a.N, kbeg + (kt + 1) * BK, kend);
     }
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 16) {
       bf16x8_t af[FM], bfr[FN];
 #pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const uint4 x = *(const uint4*)(As + (wm0 + i * 32 + fr) * LDK + kk + fk);
-        af[i] = __builtin_bit_cast(bf16x8_t, x);
-      }
+      for (int i = 0; i < FM; ++i)
+        af[i] = __builtin_bit_cast(bf16x8_t,
+                                   *(const uint4*)(As + lds_off(wm0 + i * 32 + fr, kk + fk)));
 #pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const uint4 x = *(const uint4*)(Bs + (wn0 + j * 32 + fr) * LDK + kk + fk);
-        bfr[j] = __builtin_bit_cast(bf16x8_t, x);
-      }
+      for (int j = 0; j < FN; ++j)
+        bfr[j] = __builtin_bit_cast(bf16x8_t,
+                                    *(const uint4*)(Bs + lds_off(wn0 + j * 32 + fr, kk + fk)));
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -224,6 +231,7 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(GemmArgs a) {
   }
   // acc[i][j][v] holds D[row][col] of the 32x32 tile with
   // row = 8 (v / 4) + 4 (lane / 32) + v % 4, col = lane % 32
+  float* part = SPLIT ? a.ws + (long)blockIdx.z * a.M * a.N : nullptr;
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -232,33 +240,104 @@ __global__ __launch_bounds__(NT) void gemm_mfma_kernel(GemmArgs a) {
       for (int v = 0; v < 16; ++v) {
         const int m = m0 + wm0 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
         const int n = n0 + wn0 + j * 32 + (lane & 31);
-        if (m < a.M && n < a.N) epi_store<bf16, EPI>(a, m, n, acc[i][j][v]);
+        if (m < a.M && n < a.N) {
+          if constexpr (SPLIT)
+            part[(long)m * a.N + n] = acc[i][j][v];
+          else
+            epi_store<bf16, EPI>(a, m, n, acc[i][j][v]);
+        }
       }
 }
 
-template <int BM, int BN, bool A_KC, bool B_KC>
+// Sums the split partials in split order (deterministic) and applies the epilogue.
+template <int EPI>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
+  const long tot = (long)a.M * a.N;
+  for (long e = (long)blockIdx.x * 256 + threadIdx.x; e < tot; e += (long)gridDim.x * 256) {
+    float s = 0.f;
+    for (int z = 0; z < a.splits; ++z) s += a.ws[(long)z * tot + e];
+    epi_store<bf16, EPI>(a, (int)(e / a.N), (int)(e % a.N), s);
+  }
+}
+
+template <int BM, int BN, int WGM, int WGN, bool A_KC, bool B_KC, bool SPLIT>
 hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
-  dim3 grid(cdiv(a.N, BN), cdiv(a.M, BM));
+  dim3 grid(cdiv(a.N, BN), cdiv(a.M, BM), SPLIT ? a.splits : 1);
+  constexpr int NTH = 64 * WGM * WGN;
+  if constexpr (SPLIT) {
+    gemm_mfma_kernel<BM, BN, WGM, WGN, A_KC, B_KC, EPI_STORE, true><<<grid, NTH, 0, s>>>(a);
+  } else {
+    switch (a.epi) {
+#define TP_CASE(E) \
+  case E: gemm_mfma_kernel<BM, BN, WGM, WGN, A_KC, B_KC, E, false><<<grid, NTH, 0, s>>>(a); break;
+      TP_CASE(EPI_STORE)
+      TP_CASE(EPI_QKV)
+      TP_CASE(EPI_RESID)
+      TP_CASE(EPI_GELU)
+      TP_CASE(EPI_DGELU)
+      TP_CASE(EPI_ACC_F32)
+#undef TP_CASE
+      default: return hipErrorInvalidValue;
+    }
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce(const GemmArgs& a, hipStream_t s) {
+  const long tot = (long)a.M * a.N;
+  const int blocks = (int)std::min<long>(cdiv(tot, 256), 4096);
   switch (a.epi) {
-    case EPI_STORE: gemm_mfma_kernel<BM, BN, A_KC, B_KC, EPI_STORE><<<grid, NT, 0, s>>>(a); break;
-    case EPI_QKV: gemm_mfma_kernel<BM, BN, A_KC, B_KC, EPI_QKV><<<grid, NT, 0, s>>>(a); break;
-    case EPI_RESID: gemm_mfma_kernel<BM, BN, A_KC, B_KC, EPI_RESID><<<grid, NT, 0, s>>>(a); break;
-    case EPI_GELU: gemm_mfma_kernel<BM, BN, A_KC, B_KC, EPI_GELU><<<grid, NT, 0, s>>>(a); break;
-    case EPI_DGELU: gemm_mfma_kernel<BM, BN, A_KC, B_KC, EPI_DGELU><<<grid, NT, 0, s>>>(a); break;
-    case EPI_ACC_F32:
-      gemm_mfma_kernel<BM, BN, A_KC, B_KC, EPI_ACC_F32><<<grid, NT, 0, s>>>(a);
-      break;
+#define TP_CASE(E) \
+  case E: splitk_reduce_kernel<E><<<blocks, 256, 0, s>>>(a); break;
+    TP_CASE(EPI_STORE)
+    TP_CASE(EPI_QKV)
+    TP_CASE(EPI_RESID)
+    TP_CASE(EPI_GELU)
+    TP_CASE(EPI_DGELU)
+    TP_CASE(EPI_ACC_F32)
+#undef TP_CASE
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
+// Tile choice and split-K.  Slice-shaped products (M <= 256 tokens) take all
+// rows in one block so every weight byte is fetched once; products over a
+// whole sequence use 128 x 128 blocks.  Split-K raises the workgroup count to
+// about three per CU while keeping >= 8 k-tiles per split.
+template <int BM, int BN, int WGM, int WGN, bool A_KC, bool B_KC>
+hipError_t run_cfg(GemmArgs a, hipStream_t s) {
+  constexpr int TARGET_WGS = 768;
+  const long tiles = (long)cdiv(a.M, BM) * cdiv(a.N, BN);
+  int splits = 1;
+  if (tiles < TARGET_WGS && a.ws) {
+    splits = (int)std::min<long>(8, cdiv(TARGET_WGS, tiles));
+    while (splits > 1 && (a.K / splits < 8 * BK || (long)splits * a.M * a.N > a.ws_elems))
+      --splits;
+  }
+  if (splits > 1) {
+    a.k_split = cdiv(cdiv(a.K, splits), BK) * BK;
+    a.splits = cdiv(a.K, a.k_split);
+    hipError_t e = launch_cfg<BM, BN, WGM, WGN, A_KC, B_KC, true>(a, s);
+    if (e != hipSuccess) return e;
+    return launch_reduce(a, s);
+  }
+  return launch_cfg<BM, BN, WGM, WGN, A_KC, B_KC, false>(a, s);
+}
+
 template <bool A_KC, bool B_KC>
 hipError_t launch_layout(const GemmArgs& a, hipStream_t s) {
-  if (a.M <= 64) return launch_cfg<64, 128, A_KC, B_KC>(a, s);
-  if (a.M <= 128) return launch_cfg<128, 128, A_KC, B_KC>(a, s);
-  return launch_cfg<256, 128, A_KC, B_KC>(a, s);
+  if (a.M <= 64) return run_cfg<64, 128, 1, 2, A_KC, B_KC>(a, s);
+  if (a.M <= 128) return run_cfg<128, 128, 2, 2, A_KC, B_KC>(a, s);
+  if (a.M <= 256) return run_cfg<256, 128, 4, 2, A_KC, B_KC>(a, s);
+  return run_cfg<128, 128, 2, 2, A_KC, B_KC>(a, s);
 }
+
+}  // namespace
+
+hipError_t gemm_splitk_reduce(const GemmArgs& a, hipStream_t s) { return launch_reduce(a, s); }
+
+namespace {
 
 inline bool al16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 

@@ -1,0 +1,433 @@
+// bf16 GEMM for k-aligned shapes: global -> LDS by the CDNA4 LDS DMA
+// (global_load_lds_dwordx4, 16 bytes per lane straight into LDS), a ring of
+// STAGES k-tiles in flight, and matrix-core reads straight from LDS:
+//  - k-contiguous operand tiles ([row][64 k], 128-byte rows) are read with
+//    ds_read_b128 (8 consecutive k for one row);
+//  - operands contiguous along m/n stay in their global orientation in LDS
+//    ([64 k][R], k-major) and are read with two ds_read_b64_tr_b16, the
+//    transposing LDS read: within each 16-lane group, lane j addresses 4
+//    consecutive columns of row k0 + j/4, and lane i receives column i of the
+//    group's 16 columns at the 4 rows -- exactly 4 reduction values of one
+//    MFMA row/column.
+// Both layouts permute 16-byte chunks by an XOR of the row so that the DMA
+// writes stay contiguous and the fragment reads avoid bank conflicts; the
+// DMA lane order implements the permutation (each lane picks the global chunk
+// that belongs at its LDS slot).
+//
+// LDS reads are issued as inline assembly with explicit lgkmcnt waits, and the
+// DMA completion with explicit vmcnt waits before each barrier, so the
+// compiler's conservative wait-for-all-DMA before LDS reads does not serialise
+// the pipeline.
+#include <algorithm>
+
+#include "tp_common.hpp"
+#include "tp_kernels.hpp"
+
+namespace tp {
+
+hipError_t gemm_splitk_reduce(const GemmArgs& a, hipStream_t s);
+
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ inline uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// k-contiguous tile of BK k per row: row r, 16-byte chunk c (k = 8c..8c+7) at
+// r*2BK + 16*(c ^ swz_kc(r)).  Any 16 consecutive rows read at one chunk land
+// on 16 distinct 16-byte bank groups.
+template <int BK>
+__device__ inline int swz_kc(int r) {
+  if constexpr (BK == 64) return (r ^ (r >> 3)) & 7;
+  else return (r >> 2) & 3;
+}
+// m/n-contiguous tile of R columns: k-row k, 16-byte chunk c at k*2R + 16*(c ^ swz_mc(k)).
+__device__ inline int swz_mc(int k) { return (k & 3) << 2; }
+
+template <typename T, int EPI>
+__device__ inline void epi_store(const GemmArgs& a, int m, int n, float acc) {
+  if constexpr (EPI == EPI_ACC_F32) {
+    float* C = (float*)a.C + (long)m * a.ldc + n;
+    *C += acc;
+  } else if constexpr (EPI == EPI_DGELU) {
+    const float z = ld((const T*)a.R + (long)m * a.ldr + n);
+    st((T*)a.C + (long)m * a.ldc + n, acc * gelu_tanh_grad(z));
+  } else {
+    const float v = acc + (a.bias ? ld((const T*)a.bias + n) : 0.f);
+    if constexpr (EPI == EPI_STORE) {
+      st((T*)a.C + (long)m * a.ldc + n, v);
+    } else if constexpr (EPI == EPI_RESID) {
+      st((T*)a.C + (long)m * a.ldc + n, v + ld((const T*)a.R + (long)m * a.ldr + n));
+    } else if constexpr (EPI == EPI_GELU) {
+      st((T*)a.C + (long)m * a.ldc + n, v);
+      st((T*)a.C2 + (long)m * a.ldc2 + n, gelu_tanh(v));
+    } else if constexpr (EPI == EPI_QKV) {
+      const int H = a.H;
+      if (n < H)
+        st((T*)a.q + (long)m * H + n, v);
+      else if (n < 2 * H)
+        st((T*)a.k + (long)m * H + (n - H), v);
+      else
+        st((T*)a.v + (long)m * H + (n - 2 * H), v);
+    }
+  }
+}
+
+__device__ inline void dma16(const uint16_t* g, uint16_t* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
+                                   (__attribute__((address_space(3))) void*)lds_wave_base, 16, 0,
+                                   0);
+}
+
+// Issue the DMA of one R x 64 operand tile into LDS (tile base `lds`).
+// KC: X(r, k) = X[r * ld + k]; MC: X(r, k) = X[k * ld + r].  Rows/columns past
+// rmax are clamped to valid memory (their products are never stored); k is
+// always in range (the caller guarantees whole k-tiles).
+template <int R, int BK, int NTH, bool KC>
+__device__ inline void dma_tile(const uint16_t* X, long ld, int r0, int rmax, int k0,
+                                uint16_t* lds) {
+  constexpr int CH = R * BK / 8 / NTH;  // 16-byte chunks per thread
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < CH; ++i) {
+    const int s = i * NTH + w * 64 + lane;  // LDS slot of this lane
+    const uint16_t* g;
+    if constexpr (KC) {
+      constexpr int CPR = BK / 8;  // chunks per row
+      const int row = s / CPR, phys = s % CPR;
+      const int logical = phys ^ swz_kc<BK>(row);
+      const int gr = min(r0 + row, rmax - 1);
+      g = X + (long)gr * ld + k0 + logical * 8;
+    } else {
+      constexpr int CPR = R / 8;  // chunks per k-row
+      const int krow = s / CPR, phys = s % CPR;
+      const int logical = phys ^ swz_mc(krow);
+      const int gc = min(r0 + logical * 8, rmax - 8);
+      g = X + (long)(k0 + krow) * ld + gc;
+    }
+    dma16(g, lds + (i * NTH + w * 64) * 8);
+  }
+}
+
+__device__ inline u32x4 ds_read128(uint32_t addr) {
+  u32x4 v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
+  return v;
+}
+__device__ inline u32x2 ds_read_tr(uint32_t addr) {
+  u32x2 v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(addr));
+  return v;
+}
+
+// Fragment (8 reduction values at k0 + 8 G) of operand row/column `rc` for lane
+// (G = lane / 32).  KC tiles: one 16-byte read; MC tiles: two transposing reads.
+template <int R, int BK, bool KC>
+__device__ inline u32x4 frag_read(uint32_t tile, int rc_base, int k0, int lane) {
+  if constexpr (KC) {
+    const int row = rc_base + (lane & 31), c = (k0 >> 3) + (lane >> 5);
+    return ds_read128(tile + row * (2 * BK) + ((c ^ swz_kc<BK>(row)) << 4));
+  } else {
+    const int g = lane >> 4, j = lane & 15;
+    const int col = rc_base + 16 * (g & 1) + 4 * (j & 3);
+    const int kr0 = k0 + 8 * (g >> 1) + (j >> 2);
+    u32x2 lo, hi;
+    {
+      const int kr = kr0;
+      lo = ds_read_tr(tile + kr * (2 * R) + (((col >> 3) ^ swz_mc(kr)) << 4) + ((col & 7) << 1));
+    }
+    {
+      const int kr = kr0 + 4;
+      hi = ds_read_tr(tile + kr * (2 * R) + (((col >> 3) ^ swz_mc(kr)) << 4) + ((col & 7) << 1));
+    }
+    u32x4 r;
+    r.x = lo.x;
+    r.y = lo.y;
+    r.z = hi.x;
+    r.w = hi.y;
+    return r;
+  }
+}
+
+template <int N>
+__device__ inline void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Wait until at most `pending` k-tiles (LPT DMA instructions each) are in flight.
+template <int LPT, int MAXP>
+__device__ inline void wait_tiles(int pending) {
+  if constexpr (MAXP >= 1) {
+    if (pending >= MAXP) {
+      wait_vm<LPT * MAXP>();
+      return;
+    }
+    wait_tiles<LPT, MAXP - 1>(pending);
+  } else {
+    wait_vm<0>();
+  }
+}
+
+template <int BM, int BN, int BK, int WGM, int WGN, bool A_KC, bool B_KC, int EPI, bool SPLIT,
+          int STAGES>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
+  constexpr int NTH = 64 * WGM * WGN;
+  constexpr int WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
+  constexpr int TILE_A = BM * BK, TILE_B = BN * BK, STAGE = TILE_A + TILE_B;  // elements
+  constexpr int LPT = BK * (BM + BN) / 8 / NTH;  // DMA instructions per thread per k-tile
+  static_assert(FM >= 1 && FN >= 1, "wave tile below 32 x 32");
+  static_assert((BK * BM / 8) % NTH == 0 && (BK * BN / 8) % NTH == 0, "uneven DMA split");
+  static_assert(LPT * (STAGES - 2) <= 63, "vmcnt range");
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+
+  const uint16_t* A = (const uint16_t*)a.A;
+  const uint16_t* B = (const uint16_t*)a.B;
+  const long lda = A_KC ? a.sam : a.sak;
+  const long ldb = B_KC ? a.sbn : a.sbk;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm0 = (wave / WGN) * WM, wn0 = (wave % WGN) * WN;
+  const int kbeg = SPLIT ? blockIdx.z * a.k_split : 0;
+  const int kend = SPLIT ? min(a.K, kbeg + a.k_split) : a.K;
+  const int nk = (kend - kbeg) / BK;
+  const uint32_t sbase = lds_addr(smem);
+
+  auto issue = [&](int stage, int kt) {
+    uint16_t* st = smem + stage * STAGE;
+    dma_tile<BM, BK, NTH, A_KC>(A, lda, m0, a.M, kbeg + kt * BK, st);
+    dma_tile<BN, BK, NTH, B_KC>(B, ldb, n0, a.N, kbeg + kt * BK, st + TILE_A);
+  };
+
+  f32x16_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nk) issue(s, s);
+
+  for (int kt = 0; kt < nk; ++kt) {
+    // k-tiles kt+1 .. kt+STAGES-2 may still be in flight; tile kt must have landed
+    const int pending = min(STAGES - 2, nk - 1 - kt);
+    wait_tiles<LPT, STAGES - 2>(pending);
+    __builtin_amdgcn_s_barrier();
+    if (kt + STAGES - 1 < nk) issue((kt + STAGES - 1) % STAGES, kt + STAGES - 1);
+
+    const uint32_t ta = sbase + (kt % STAGES) * STAGE * 2;
+    const uint32_t tb = ta + TILE_A * 2;
+    u32x4 fa[2][FM], fb[2][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) fa[0][i] = frag_read<BM, BK, A_KC>(ta, wm0 + 32 * i, 0, lane);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) fb[0][j] = frag_read<BN, BK, B_KC>(tb, wn0 + 32 * j, 0, lane);
+    // first fragments: wait, with every fragment register tied to the wait
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(fa[0][0]));
+#pragma unroll
+    for (int i = 1; i < FM; ++i) asm volatile("" : "+v"(fa[0][i]));
+#pragma unroll
+    for (int j = 0; j < FN; ++j) asm volatile("" : "+v"(fb[0][j]));
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int cur = ks & 1, nxt = cur ^ 1;
+      if (ks + 1 < BK / 16) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+          fa[nxt][i] = frag_read<BM, BK, A_KC>(ta, wm0 + 32 * i, 16 * (ks + 1), lane);
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          fb[nxt][j] = frag_read<BN, BK, B_KC>(tb, wn0 + 32 * j, 16 * (ks + 1), lane);
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8_t, fa[cur][i]), __builtin_bit_cast(bf16x8_t, fb[cur][j]),
+              acc[i][j], 0, 0, 0);
+      if (ks + 1 < BK / 16) {
+        // the next fragments must have arrived (their registers are tied to the wait)
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(fa[nxt][0]));
+#pragma unroll
+        for (int i = 1; i < FM; ++i) asm volatile("" : "+v"(fa[nxt][i]));
+#pragma unroll
+        for (int j = 0; j < FN; ++j) asm volatile("" : "+v"(fb[nxt][j]));
+      }
+    }
+  }
+  // every outstanding DMA has been waited for: the last iteration waited for 0
+
+  if constexpr (SPLIT || EPI == EPI_ACC_F32) {
+    // fp32 outputs: each 32 x 32 sub-tile goes through a wave-private LDS patch
+    // (in the stage no wave reads in the last iteration) and leaves as 16-byte
+    // row segments, two lanes per row.
+    static_assert(WGM * WGN * 32 * 36 * 4 <= STAGE * 2, "epilogue patch exceeds a stage");
+    float* patch = (float*)(smem + (nk % STAGES) * STAGE) + wave * (32 * 36);
+    float* out = SPLIT ? a.ws + (long)blockIdx.z * a.M * a.N : (float*)a.C;
+    const long ldo = SPLIT ? a.N : a.ldc;
+    const int pr = lane >> 1, pc = (lane & 1) * 16;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          patch[(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * 36 + (lane & 31)] = acc[i][j][v];
+        const int m = m0 + wm0 + i * 32 + pr;
+        const int n = n0 + wn0 + j * 32 + pc;
+        float4 x[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) x[q] = *(const float4*)(patch + pr * 36 + pc + 4 * q);
+        if (m < a.M) {
+          float* dst = out + (long)m * ldo + n;
+          if (n + 16 <= a.N) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              if constexpr (!SPLIT) {
+                const float4 o = *(const float4*)(dst + 4 * q);
+                x[q].x += o.x, x[q].y += o.y, x[q].z += o.z, x[q].w += o.w;
+              }
+              *(float4*)(dst + 4 * q) = x[q];
+            }
+          } else {
+            const float* xs = (const float*)x;
+            for (int e = 0; e < 16 && n + e < a.N; ++e) dst[e] = SPLIT ? xs[e] : dst[e] + xs[e];
+          }
+        }
+      }
+  } else {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int m = m0 + wm0 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+          const int n = n0 + wn0 + j * 32 + (lane & 31);
+          if (m < a.M && n < a.N) epi_store<bf16, EPI>(a, m, n, acc[i][j][v]);
+        }
+  }
+}
+
+template <int BM, int BN, int BK, int WGM, int WGN, bool A_KC, bool B_KC, int STAGES, bool SPLIT>
+hipError_t launch_dma(const GemmArgs& a, hipStream_t s) {
+  constexpr int NTH = 64 * WGM * WGN;
+  constexpr size_t lds = (size_t)STAGES * (BM + BN) * BK * 2;
+  dim3 grid(cdiv(a.N, BN), cdiv(a.M, BM), SPLIT ? a.splits : 1);
+#define TP_LAUNCH(E)                                                                         \
+  do {                                                                                       \
+    auto* fn = gemm_dma_kernel<BM, BN, BK, WGM, WGN, A_KC, B_KC, E, SPLIT, STAGES>;        \
+    static bool attr = false;                                                                \
+    if (!attr) {                                                                             \
+      hipError_t e = hipFuncSetAttribute((const void*)fn,                                    \
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds); \
+      if (e != hipSuccess) return e;                                                         \
+      attr = true;                                                                           \
+    }                                                                                        \
+    fn<<<grid, NTH, lds, s>>>(a);                                                            \
+  } while (0)
+  if constexpr (SPLIT) {
+    TP_LAUNCH(EPI_STORE);
+  } else {
+    switch (a.epi) {
+      case EPI_STORE: TP_LAUNCH(EPI_STORE); break;
+      case EPI_QKV: TP_LAUNCH(EPI_QKV); break;
+      case EPI_RESID: TP_LAUNCH(EPI_RESID); break;
+      case EPI_GELU: TP_LAUNCH(EPI_GELU); break;
+      case EPI_DGELU: TP_LAUNCH(EPI_DGELU); break;
+      case EPI_ACC_F32: TP_LAUNCH(EPI_ACC_F32); break;
+      default: return hipErrorInvalidValue;
+    }
+  }
+#undef TP_LAUNCH
+  return hipGetLastError();
+}
+
+
+// One DMA GEMM launch.  Every configuration holds one workgroup per CU (its
+// LDS ring takes most of the 160 KB), so when the tile count is low the
+// reduction is split (<= 8 splits of >= 8 k-tiles; whole k-tiles, the last
+// split may be shorter) by the cost model below.
+template <int BM, int BN, int BK, int WGM, int WGN, bool A_KC, bool B_KC, int STAGES>
+hipError_t run_dma(GemmArgs a, hipStream_t s) {
+  constexpr int CUS = 256;
+  if (a.K % BK) return hipErrorNotSupported;
+  const long tiles = (long)cdiv(a.M, BM) * cdiv(a.N, BN);
+  const int nkt = a.K / BK;
+  int splits = 1;
+  if (a.ws && tiles < 2 * CUS) {
+    // time ~ rounds(s) / s of the unsplit main loop, plus the partial-sum
+    // traffic (s fp32 products written and read back), which relative to the
+    // weight stream of one round is about 2.2 M / K per split
+    const double lam = 2.2 * (double)a.M / (double)a.K;
+    double best = 1e30;
+    for (int sp = 1; sp <= 8; ++sp) {
+      if (sp > 1 && (nkt / sp < 8 || (long)sp * a.M * a.N > a.ws_elems)) break;
+      const long wgs = tiles * sp;
+      const double cost = (double)cdiv(wgs, CUS) / sp + (sp > 1 ? lam * sp : 0.0);
+      if (cost < best - 1e-9) {
+        best = cost;
+        splits = sp;
+      }
+    }
+  }
+  if (splits > 1) {
+    a.k_split = cdiv(nkt, splits) * BK;
+    a.splits = cdiv(a.K, a.k_split);
+    hipError_t e = launch_dma<BM, BN, BK, WGM, WGN, A_KC, B_KC, STAGES, true>(a, s);
+    if (e != hipSuccess) return e;
+    return gemm_splitk_reduce(a, s);
+  }
+  return launch_dma<BM, BN, BK, WGM, WGN, A_KC, B_KC, STAGES, false>(a, s);
+}
+
+template <bool A_KC, bool B_KC>
+hipError_t run_cfg_id(int cfg, const GemmArgs& a, hipStream_t s) {
+  switch (cfg) {
+    case 0: return run_dma<128, 128, 64, 2, 2, A_KC, B_KC, 4>(a, s);
+    case 1: return run_dma<256, 128, 64, 4, 2, A_KC, B_KC, 3>(a, s);
+    case 2: return run_dma<256, 256, 64, 2, 4, A_KC, B_KC, 2>(a, s);
+    default: return hipErrorNotSupported;
+  }
+}
+
+}  // namespace
+
+// Explicit configuration (for measurement); -1 picks by shape.  Shapes the
+// DMA path takes: K a multiple of BK; every operand dimension a multiple of 8;
+// m/n-contiguous operands at least 128 wide.
+hipError_t gemm_dma_bf16_cfg(int cfg, const GemmArgs& a, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  if (a.M % 8 || a.N % 8 || a.K % 32) return hipErrorNotSupported;
+  const bool a_kc = a.sak == 1, b_kc = a.sbk == 1, a_mc = a.sam == 1, b_nc = a.sbn == 1;
+  if (((uintptr_t)a.A & 15) || ((uintptr_t)a.B & 15)) return hipErrorNotSupported;
+  const long lda = a_kc ? a.sam : a.sak, ldb = b_kc ? a.sbn : a.sbk;
+  if ((lda & 7) || (ldb & 7)) return hipErrorNotSupported;
+  if (cfg < 0) {
+    // measured on the stage shapes: 256 x 256 tiles (2 stages) everywhere except
+    // small row counts and wide forward outputs, which prefer 256 x 128 (3 stages)
+    if (a_mc && b_nc) cfg = 2;
+    else if (a.M <= 128) cfg = 0;
+    else if (a_kc && b_kc && a.M <= 256 && a.N >= 4 * a.K) cfg = 1;
+    else cfg = 2;
+  }
+  if (a_kc && b_kc) return run_cfg_id<true, true>(cfg, a, s);
+  if (a_kc && b_nc) return run_cfg_id<true, false>(cfg, a, s);
+  if (a_mc && b_nc) {
+    if (a.M < 128 || a.N < 128) return hipErrorNotSupported;
+    return run_cfg_id<false, false>(cfg, a, s);
+  }
+  return hipErrorNotSupported;
+}
+
+hipError_t gemm_dma_bf16(const GemmArgs& a, hipStream_t s) { return gemm_dma_bf16_cfg(-1, a, s); }
+
+}  // namespace tp

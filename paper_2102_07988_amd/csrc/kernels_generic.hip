@@ -232,26 +232,75 @@ hipError_t attn_bwd_generic(int dtype, const AttnArgs& a, hipStream_t s) {
 
 // ------------------------------------------------------------- LayerNorm
 
+// 8 consecutive elements <-> 8 floats (16-byte loads for bf16, 2 x 16 for fp32).
+__device__ inline void load8(const bf16* p, float* v) {
+  const uint4 u = *(const uint4*)p;
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(w[i] << 16);
+    v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+__device__ inline void load8(const float* p, float* v) {
+  const float4 a = ((const float4*)p)[0], b = ((const float4*)p)[1];
+  v[0] = a.x, v[1] = a.y, v[2] = a.z, v[3] = a.w, v[4] = b.x, v[5] = b.y, v[6] = b.z, v[7] = b.w;
+}
+__device__ inline void store8(bf16* p, const float* v) {
+  uint4 u;
+  u.x = f32_to_bf16_bits(v[0]) | ((uint32_t)f32_to_bf16_bits(v[1]) << 16);
+  u.y = f32_to_bf16_bits(v[2]) | ((uint32_t)f32_to_bf16_bits(v[3]) << 16);
+  u.z = f32_to_bf16_bits(v[4]) | ((uint32_t)f32_to_bf16_bits(v[5]) << 16);
+  u.w = f32_to_bf16_bits(v[6]) | ((uint32_t)f32_to_bf16_bits(v[7]) << 16);
+  *(uint4*)p = u;
+}
+__device__ inline void store8(float* p, const float* v) {
+  ((float4*)p)[0] = make_float4(v[0], v[1], v[2], v[3]);
+  ((float4*)p)[1] = make_float4(v[4], v[5], v[6], v[7]);
+}
+
+// One block of 256 threads per row; the row stays in registers (H <= 16384,
+// H % 8 == 0): thread t owns the 8-element chunks t, t + 256, ...
+constexpr int LN_MAXC = 8;
+
 template <typename T>
 __global__ __launch_bounds__(256) void ln_fwd_kernel(int H, const T* x, T* x_copy, const T* g,
                                                      const T* b, T* u, float* mean, float* rstd,
                                                      float eps) {
   __shared__ float red[16];
-  const int row = blockIdx.x;
+  const int row = blockIdx.x, nc = H >> 3;
   const T* xr = x + (long)row * H;
+  float v[LN_MAXC][8];
   float s = 0.f;
-  for (int i = threadIdx.x; i < H; i += blockDim.x) s += ld(xr + i);
-  const float mu = block_sum(s, red) / H;
-  float v = 0.f;
-  for (int i = threadIdx.x; i < H; i += blockDim.x) {
-    const float c = ld(xr + i) - mu;
-    v += c * c;
+#pragma unroll
+  for (int c = 0; c < LN_MAXC; ++c) {
+    const int ci = threadIdx.x + 256 * c;
+    if (ci < nc) {
+      load8(xr + ci * 8, v[c]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s += v[c][e];
+    }
   }
-  const float rs = rsqrtf(block_sum(v, red) / H + eps);
-  for (int i = threadIdx.x; i < H; i += blockDim.x) {
-    const float xv = ld(xr + i);
-    st(u + (long)row * H + i, ld(g + i) * ((xv - mu) * rs) + ld(b + i));
-    if (x_copy) x_copy[(long)row * H + i] = xr[i];
+  const float mu = block_sum(s, red) / H;
+  float q = 0.f;
+#pragma unroll
+  for (int c = 0; c < LN_MAXC; ++c)
+    if (threadIdx.x + 256 * c < nc)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) q += (v[c][e] - mu) * (v[c][e] - mu);
+  const float rs = rsqrtf(block_sum(q, red) / H + eps);
+#pragma unroll
+  for (int c = 0; c < LN_MAXC; ++c) {
+    const int ci = threadIdx.x + 256 * c;
+    if (ci < nc) {
+      float gg[8], bb[8], o[8];
+      load8(g + ci * 8, gg);
+      load8(b + ci * 8, bb);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = gg[e] * ((v[c][e] - mu) * rs) + bb[e];
+      store8(u + (long)row * H + ci * 8, o);
+      if (x_copy) store8(x_copy + (long)row * H + ci * 8, v[c]);
+    }
   }
   if (threadIdx.x == 0) {
     mean[row] = mu;
@@ -264,52 +313,113 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(int H, const T* du, const T
                                                      const float* mean, const float* rstd,
                                                      const T* g, const T* resid, T* dx) {
   __shared__ float red[16];
-  const int row = blockIdx.x;
+  const int row = blockIdx.x, nc = H >> 3;
   const float mu = mean[row], rs = rstd[row];
+  float xh[LN_MAXC][8], dg[LN_MAXC][8];
   float sa = 0.f, sb = 0.f;
-  for (int i = threadIdx.x; i < H; i += blockDim.x) {
-    const float xh = (ld(x + (long)row * H + i) - mu) * rs;
-    const float dxh = ld(du + (long)row * H + i) * ld(g + i);
-    sa += dxh;
-    sb += dxh * xh;
+#pragma unroll
+  for (int c = 0; c < LN_MAXC; ++c) {
+    const int ci = threadIdx.x + 256 * c;
+    if (ci < nc) {
+      float d[8], gg[8];
+      load8(x + (long)row * H + ci * 8, xh[c]);
+      load8(du + (long)row * H + ci * 8, d);
+      load8(g + ci * 8, gg);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        xh[c][e] = (xh[c][e] - mu) * rs;
+        dg[c][e] = d[e] * gg[e];
+        sa += dg[c][e];
+        sb += dg[c][e] * xh[c][e];
+      }
+    }
   }
   const float a = block_sum(sa, red) / H;
-  const float b = block_sum(sb, red) / H;
-  for (int i = threadIdx.x; i < H; i += blockDim.x) {
-    const float xh = (ld(x + (long)row * H + i) - mu) * rs;
-    float v = rs * (ld(du + (long)row * H + i) * ld(g + i) - a - xh * b);
-    if (resid) v += ld(resid + (long)row * H + i);
-    st(dx + (long)row * H + i, v);
+  const float bm = block_sum(sb, red) / H;
+#pragma unroll
+  for (int c = 0; c < LN_MAXC; ++c) {
+    const int ci = threadIdx.x + 256 * c;
+    if (ci < nc) {
+      float o[8], r[8];
+      if (resid) load8(resid + (long)row * H + ci * 8, r);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = rs * (dg[c][e] - a - xh[c][e] * bm) + (resid ? r[e] : 0.f);
+      store8(dx + (long)row * H + ci * 8, o);
+    }
   }
 }
 
-// Column reductions: each block owns 256 consecutive columns and loops over
-// all rows in order, so results are deterministic.
+// Column reductions: a block owns 64 columns (8 chunks of 8) and 32 row groups;
+// row group rg sums rows rg, rg + 32, ... in order, then the 32 partial sums
+// are added in row-group order.  Deterministic.
 template <typename T>
 __global__ __launch_bounds__(256) void ln_param_grads_kernel(int n, int H, const T* du,
                                                              const T* x, const float* mean,
                                                              const float* rstd, float* dg,
                                                              float* db) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= H) return;
-  float sg = 0.f, sb = 0.f;
-  for (int t = 0; t < n; ++t) {
-    const float d = ld(du + (long)t * H + i);
-    sg += d * ((ld(x + (long)t * H + i) - mean[t]) * rstd[t]);
-    sb += d;
+  __shared__ float pg[32][65], pb[32][65];
+  const int cc = threadIdx.x & 7, rg = threadIdx.x >> 3;
+  const int c0 = blockIdx.x * 64 + cc * 8;
+  float sg[8] = {}, sb[8] = {};
+  if (c0 < H) {
+    for (int t = rg; t < n; t += 32) {
+      float d[8], xv[8];
+      load8(du + (long)t * H + c0, d);
+      load8(x + (long)t * H + c0, xv);
+      const float mu = mean[t], rs = rstd[t];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        sg[e] += d[e] * ((xv[e] - mu) * rs);
+        sb[e] += d[e];
+      }
+    }
   }
-  dg[i] += sg;
-  db[i] += sb;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    pg[rg][cc * 8 + e] = sg[e];
+    pb[rg][cc * 8 + e] = sb[e];
+  }
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    const int col = blockIdx.x * 64 + threadIdx.x;
+    if (col < H) {
+      float a = 0.f, b = 0.f;
+      for (int r = 0; r < 32; ++r) {
+        a += pg[r][threadIdx.x];
+        b += pb[r][threadIdx.x];
+      }
+      dg[col] += a;
+      db[col] += b;
+    }
+  }
 }
 
 template <typename T>
 __global__ __launch_bounds__(256) void colsum_kernel(int n, int N, const T* A, long lda,
                                                      float* out) {
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= N) return;
-  float s = 0.f;
-  for (int t = 0; t < n; ++t) s += ld(A + (long)t * lda + j);
-  out[j] += s;
+  __shared__ float ps[32][65];
+  const int cc = threadIdx.x & 7, rg = threadIdx.x >> 3;
+  const int c0 = blockIdx.x * 64 + cc * 8;
+  float s[8] = {};
+  if (c0 < N) {
+    for (int t = rg; t < n; t += 32) {
+      float v[8];
+      load8(A + (long)t * lda + c0, v);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s[e] += v[e];
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ps[rg][cc * 8 + e] = s[e];
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    const int col = blockIdx.x * 64 + threadIdx.x;
+    if (col < N) {
+      float a = 0.f;
+      for (int r = 0; r < 32; ++r) a += ps[r][threadIdx.x];
+      out[col] += a;
+    }
+  }
 }
 
 template <typename T>
@@ -363,10 +473,10 @@ hipError_t ln_param_grads(int dtype, int n, int H, const void* du, const void* x
                           hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if (dtype == DT_FP32)
-    ln_param_grads_kernel<float><<<cdiv(H, 256), 256, 0, s>>>(n, H, (const float*)du,
+    ln_param_grads_kernel<float><<<cdiv(H, 64), 256, 0, s>>>(n, H, (const float*)du,
                                                                (const float*)x, mean, rstd, dg, db);
   else
-    ln_param_grads_kernel<bf16><<<cdiv(H, 256), 256, 0, s>>>(n, H, (const bf16*)du,
+    ln_param_grads_kernel<bf16><<<cdiv(H, 64), 256, 0, s>>>(n, H, (const bf16*)du,
                                                               (const bf16*)x, mean, rstd, dg, db);
   return hipGetLastError();
 }
@@ -375,9 +485,9 @@ hipError_t colsum_acc(int dtype, int n, int N, const void* A, long lda, float* o
                       hipStream_t s) {
   if (n <= 0 || N <= 0) return hipSuccess;
   if (dtype == DT_FP32)
-    colsum_kernel<float><<<cdiv(N, 256), 256, 0, s>>>(n, N, (const float*)A, lda, out);
+    colsum_kernel<float><<<cdiv(N, 64), 256, 0, s>>>(n, N, (const float*)A, lda, out);
   else
-    colsum_kernel<bf16><<<cdiv(N, 256), 256, 0, s>>>(n, N, (const bf16*)A, lda, out);
+    colsum_kernel<bf16><<<cdiv(N, 64), 256, 0, s>>>(n, N, (const bf16*)A, lda, out);
   return hipGetLastError();
 }
 

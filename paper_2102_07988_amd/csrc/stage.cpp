@@ -32,6 +32,8 @@ struct Scratch {
   void *du2, *du, *dout;  // [Lmax][H]
   float* D;               // [heads][Lmax]
   void *io_a, *io_b;      // profiler slice buffers [Lmax][H]
+  float* splitk;          // split-K partial sums of the slice GEMMs
+  size_t splitk_elems;
 };
 
 struct Carver {
@@ -92,7 +94,7 @@ bool config_ok(const tp_stage_config* c) {
 bool config_supported(const tp_stage_config* c) {
   const int d = c->hidden / c->heads;
   if (d != 16 && d != 32 && d != 64 && d != 128) return false;
-  if (c->hidden % 8) return false;
+  if (c->hidden % 8 || c->hidden > 16384) return false;  // LayerNorm rows live in registers
   // the generic attention keeps one score row per block in LDS
   if ((2 * (size_t)c->max_seq + 272) * 4 > 160 * 1024) return false;
   return true;
@@ -134,6 +136,9 @@ size_t carve(const tp_stage_config* c, void* base, std::vector<LayerBufs>* lbs, 
   s.D = (float*)cv.take(a * L * 4);
   s.io_a = cv.take(L * H * esz);
   s.io_b = cv.take(L * H * esz);
+  // up to 8 partial [min(L, 256)][4H] fp32 products
+  s.splitk_elems = 8 * std::min<size_t>(L, 256) * F;
+  s.splitk = (float*)cv.take(s.splitk_elems * 4);
   if (sc) *sc = s;
   return (cv.off + 255) & ~(size_t)255;
 }
@@ -183,7 +188,9 @@ double gemm_bytes(const GemmArgs& g, size_t esz) {
   return b;
 }
 
-hipError_t run_gemm(tp_stage* S, int cls, const GemmArgs& g) {
+hipError_t run_gemm(tp_stage* S, int cls, GemmArgs g) {
+  g.ws = S->sc.splitk;
+  g.ws_elems = (long)S->sc.splitk_elems;
   return launch(S, cls, 2.0 * g.M * g.N * g.K, gemm_bytes(g, S->esz),
                 [&] { return gemm(S->dt, g, S->stream); });
 }
@@ -430,8 +437,10 @@ tp_status tp_kv_prefix_reset(tp_stage* S) {
   return TP_OK;
 }
 
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
 tp_status tp_slice_forward(tp_stage* S, int l, int r, const void* x, void* y) {
-  if (!S || !x || !y) return TP_ERR_INVALID;
+  if (!S || !x || !y || !aligned16(x) || !aligned16(y)) return TP_ERR_INVALID;
   if (l < 0 || r <= l || r > S->L) return TP_ERR_INVALID;
   if (l != S->cached_len) return TP_ERR_ORDER;
   tp_status s = forward_impl(S, l, r, x, y);
@@ -442,7 +451,7 @@ tp_status tp_slice_forward(tp_stage* S, int l, int r, const void* x, void* y) {
 }
 
 tp_status tp_slice_backward(tp_stage* S, int l, int r, const void* dy, void* dx) {
-  if (!S || !dy || !dx) return TP_ERR_INVALID;
+  if (!S || !dy || !dx || !aligned16(dy) || !aligned16(dx)) return TP_ERR_INVALID;
   if (l < 0 || r <= l || r > S->L) return TP_ERR_INVALID;
   if (r != S->bwd_frontier) return TP_ERR_ORDER;
   tp_status s = backward_impl(S, l, r, dy, dx);

@@ -37,6 +37,11 @@ struct GemmArgs {
   long ldc2 = 0;
   void *q = nullptr, *k = nullptr, *v = nullptr;  // EPI_QKV destinations, row stride H
   int H = 0;
+  // fp32 scratch for split-K partial sums (may be null: no split)
+  float* ws = nullptr;
+  long ws_elems = 0;
+  // set by the launcher: reduction range of one split and the split count
+  int k_split = 0, splits = 1;
 };
 
 hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s);

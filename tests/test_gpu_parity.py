@@ -87,3 +87,18 @@ def test_order_errors_leave_state():
     st.backward(8, 16, xd[8:16])
     st.backward(0, 8, xd[:8])
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("H,heads", [(256, 2), (256, 4)])  # d = 128, 64
+@pytest.mark.parametrize("wgrad", ["per_slice", "deferred"])
+def test_matrix_core_attention_ragged(H, heads, wgrad):
+    """bf16 head widths 64/128 (matrix-core attention): ragged slices that are not
+    multiples of any tile, a 1-token slice, and backward boundaries that differ."""
+    _case(2, H, heads, 150, "bf16", [37, 1, 29, 83], [50, 7, 93], wgrad, seeds=(11, 12, 13),
+          randomize_ln=True, label=f"mfma-attn d={H // heads}")
+
+
+def test_long_prefix_short_slices():
+    """Late slices attend to a long cached prefix (context >> slice length)."""
+    _case(1, 512, 4, 520, "bf16", [384, 16, 48, 72], [8, 512], seeds=(21, 22, 23),
+          label="long prefix")
