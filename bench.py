@@ -73,6 +73,54 @@ def cpu_baseline(params0, x, dy, hidden: int, heads: int, n_tokens: int):
                       f"{n_tokens} tokens at context 0, forward+backward, fp64"}
 
 
+def pipeline_report(st, tp, L: int, unit: int, K: int, warmup: int, reps: int,
+                    seq_ms: float, dw_ms: float):
+    """Measure the per-slice cost table t(len, ctx) = t_fwd + t_bwd on this stage
+    (lengths and contexts in multiples of `unit`), solve the optimal slicing for a
+    pipeline of K such stages (Eq. 5-8, Algorithm 1) and compare Eq. 5 latencies
+    of the DP slicing, uniform slicings and one slice."""
+    import numpy as np
+
+    U = L // unit
+    lens = [unit * k for k in range(1, U + 1)]
+    ctxs = [unit * j for j in range(U)]
+    t0 = time.perf_counter()
+    tf, tb = st.profile(lens, ctxs, warmup=warmup, reps=reps)
+    prof_s = time.perf_counter() - t0
+    cost = np.full((U, U), -1, dtype=np.int64)
+    for k in range(U):
+        for j in range(U):
+            if k + 1 + j <= U:
+                cost[k, j] = tf[k, j] + tb[k, j]
+    t1 = time.perf_counter()
+    dp_lens, dp_T = tp.dp_optimal_slicing(cost, unit, K)
+    dp_s = time.perf_counter() - t1
+
+    def eq5(units):
+        ts, c = [], 0
+        for u in units:
+            ts.append(int(cost[u - 1, c]))
+            c += u
+        return sum(ts) + (K - 1) * max(ts)
+
+    uniform = {}
+    for m in range(1, U + 1):
+        if U % m == 0:
+            uniform[str(m)] = round(eq5([U // m] * m) / 1e6, 3)
+    best_m = min(uniform, key=uniform.get)
+    return {
+        "K": K, "unit": unit, "table_points": int((cost >= 0).sum()),
+        "profile_seconds": round(prof_s, 2), "dp_seconds": round(dp_s, 4),
+        "dp_slicing": dp_lens, "dp_T_ms": round(dp_T / 1e6, 3),
+        "uniform_T_ms": uniform, "best_uniform_slices": int(best_m),
+        "dp_speedup_vs_best_uniform": round(uniform[best_m] / (dp_T / 1e6), 4),
+        "single_slice_T_ms": uniform["1"],
+        "deferred_dw_ms_per_sequence": round(dw_ms, 3),
+        "note": "T = Eq. 5 over the measured t_fwd + t_bwd table; in deferred mode the "
+                "once-per-sequence dW GEMMs (deferred_dw_ms) add to the last stage's tail",
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -84,6 +132,10 @@ def main():
     ap.add_argument("--cpu-baseline-tokens", type=int, default=48)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--no-pipeline", action="store_true",
+                    help="skip the cost-table / DP / Eq. 5 pipeline-latency report")
+    ap.add_argument("--pipeline-unit", type=int, default=128)
+    ap.add_argument("--pipeline-K", type=int, default=48)
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -176,6 +228,11 @@ def main():
         "flops_per_step": flops_step, "outputs_finite": finite,
         "roofline": roofline, "kernels": kernels,
     }
+    if not args.no_pipeline:
+        dw_ms = kernels.get("gemm_bwd_dw_tn", {}).get("ms_per_step", 0.0) if args.wgrad == "deferred" else 0.0
+        out["pipeline"] = pipeline_report(st, tp, L, args.pipeline_unit, args.pipeline_K, 1, 3,
+                                          ms, dw_ms)
+        st.zero_grads()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(params[0], x, dy, H, heads, args.cpu_baseline_tokens)
     print(json.dumps(out), flush=True)

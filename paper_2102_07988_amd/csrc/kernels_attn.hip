@@ -4,26 +4,29 @@
 // Queries t in [l, r) attend keys s <= t of the per-layer cache [0, r) (Eq. 2
 // with every earlier slice's keys/values cached).
 //
-// MFMA fragment conventions (32 x 32 x 16): a lane l = 32 G + c supplies row c
-// of the left operand and column c of the right operand, 8 values each at the
-// lane group's 8 reduction slots; the accumulator element v of lane l is
-// D[8 (v / 4) + 4 G + v % 4][c].  A score tile computed by one MFMA therefore
-// gives each lane one column and 16 rows; when those 16 values feed the next
-// MFMA as an operand, the reduction slot e of group G stands for row
-// 16 ks + (e < 4 ? 4 G + e : 8 + 4 G + e - 4) (ks = which half of the 32),
-// and the other operand is read from LDS with the same pairing.
+// MFMA fragment conventions (32 x 32 x 16): lane l = 32 G + c supplies row c of
+// the left operand and column c of the right operand, 8 values each at its
+// group's 8 reduction slots; accumulator element v of lane l is
+// D[8 (v / 4) + 4 G + v % 4][c].  A score tile computed by one MFMA thus gives
+// each lane one column and 16 rows; fed back as an operand, reduction slot e of
+// group G stands for row 16 ks + (e < 4 ? 4 G + e : 8 + 4 G + e - 4)
+// (ks = which half of the 32).  The other operand of such a product is read
+// from an LDS tile with two transposing reads (ds_read_b64_tr_b16) whose row
+// bases follow the same pairing, so tiles stay in their natural [token][d]
+// orientation in LDS.
 //
-//  forward  : S^T = K Q^T (lane = one query, so the online softmax is
-//             lane-local plus one exchange with lane ^ 32), O^T += V^T P^T.
-//  dK/dV    : one block of keys per wave; S = Q K^T and dP = dO V^T (lane =
+//  forward  : S^T = K Q^T (lane = one query: the online softmax is lane-local
+//             plus one exchange with lane ^ 32), O^T += V^T P^T.
+//  dK/dV    : one block of 32 keys per wave; S = Q K^T and dP = dO V^T (lane =
 //             one key), dV += P^T dO, dK += dS^T Q; results are added to the
 //             fp32 dK/dV buffer (each element owned by one lane: no atomics).
-//  dQ       : one block of queries per wave; S^T = K Q^T, dP^T = V dO^T,
+//  dQ       : one block of 32 queries per wave; S^T = K Q^T, dP^T = V dO^T,
 //             dQ^T += K^T dS^T.
-// Tiles that must be read along the key/query index are transposed in
-// registers on their way into LDS.
+// K/V (or Q/dO) tiles move from HBM to a double-buffered LDS ring by the LDS
+// DMA, so the next tile streams in while the current one is multiplied.
 #include "tp_common.hpp"
 #include "tp_kernels.hpp"
+#include "tp_lds.hpp"
 
 namespace tp {
 
@@ -35,8 +38,9 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 
-__device__ inline f32x16_t mfma(bf16x8_t a, bf16x8_t b, f32x16_t c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+__device__ inline f32x16_t mfma(u32x4 a, u32x4 b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                 __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
 }
 
 __device__ inline f32x16_t zero16() {
@@ -51,77 +55,68 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 // 8 accumulator values (one reduction half) as a bf16 operand.
-__device__ inline bf16x8_t acc_half_bf16(const f32x16_t& x, int ks) {
-  uint4 u;
-  if (ks == 0)
-    u = make_uint4(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(x[4], x[5]),
-                   pack_bf16x2(x[6], x[7]));
-  else
-    u = make_uint4(pack_bf16x2(x[8], x[9]), pack_bf16x2(x[10], x[11]),
-                   pack_bf16x2(x[12], x[13]), pack_bf16x2(x[14], x[15]));
-  return __builtin_bit_cast(bf16x8_t, u);
+__device__ inline u32x4 acc_half_bf16(const f32x16_t& x, int ks) {
+  u32x4 u;
+  const int o = 8 * ks;
+  u.x = pack_bf16x2(x[o + 0], x[o + 1]);
+  u.y = pack_bf16x2(x[o + 2], x[o + 3]);
+  u.z = pack_bf16x2(x[o + 4], x[o + 5]);
+  u.w = pack_bf16x2(x[o + 6], x[o + 7]);
+  return u;
 }
 
-// Operand read from a row of an LDS tile that is contiguous along the
-// reduction index, in the paired slot order: 4 values at k0 + 4G and 4 at
-// k0 + 8 + 4G.
-__device__ inline bf16x8_t lds_pair_read(const uint16_t* row, int k0, int G) {
-  const uint2 a = *(const uint2*)(row + k0 + 4 * G);
-  const uint2 b = *(const uint2*)(row + k0 + 8 + 4 * G);
-  return __builtin_bit_cast(bf16x8_t, make_uint4(a.x, a.y, b.x, b.y));
-}
-
-__device__ inline bf16x8_t lds_read16(const uint16_t* p) {
-  return __builtin_bit_cast(bf16x8_t, *(const uint4*)p);
-}
-
-// LDS[r][c] = G[r][c] (row stride ld) for r < ROWS, c < COLS; rows >= rvalid are 0.
-template <int ROWS, int COLS, int LDR, int NTH>
-__device__ inline void lds_copy(uint16_t* lds, const uint16_t* G, long ld, int rvalid) {
-  constexpr int CPR = COLS / 8, TOT = ROWS * CPR;
-#pragma unroll
-  for (int c = threadIdx.x; c < TOT; c += NTH) {
-    const int r = c / CPR, k = (c % CPR) * 8;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (r < rvalid) v = *(const uint4*)(G + (long)r * ld + k);
-    *(uint4*)(lds + r * LDR + k) = v;
+// Tile of rows x D bf16 in LDS, rows of 2D bytes whose 16-byte chunks are
+// permuted by chunk ^ f(row).  f makes both the row-fragment reads (16
+// consecutive rows at one chunk) and the transposing reads (8 rows x 4 chunks)
+// use every bank group at most twice.
+template <int D>
+struct Tile {
+  static constexpr int CPR = D / 8;
+  __device__ static int f(int r) {
+    if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+    else return (r >> 1) & 7;
   }
-}
-
-__device__ inline uint32_t word_of(const uint4& x, int w) {
-  return w == 0 ? x.x : w == 1 ? x.y : w == 2 ? x.z : x.w;
-}
-
-// LDS[c][r] = G[r][c] (transpose; LDS row stride LDR runs over r) for r < ROWS,
-// c < COLS; rows r >= rvalid are 0.  Blocks of 4 rows x 8 columns per thread.
-template <int ROWS, int COLS, int LDR, int NTH>
-__device__ inline void lds_copy_t(uint16_t* lds, const uint16_t* G, long ld, int rvalid) {
-  constexpr int CB = COLS / 8, TOT = (ROWS / 4) * CB;
-  for (int b = threadIdx.x; b < TOT; b += NTH) {
-    const int rb = b / CB, cb = b % CB;
-    uint4 x[4];
+  // byte offset of chunk c of row r
+  __device__ static uint32_t off(int r, int c) { return r * (2 * D) + ((c ^ f(r)) << 4); }
+  // 8 consecutive d values [8c, 8c+8) of row r
+  __device__ static u32x4 row8(uint32_t base, int r, int c) { return ds_read128(base + off(r, c)); }
+  // transposed operand: this lane's column cb + (lane % 32) at rows
+  // r0 + 4 G + (0..3) and r0 + 8 + 4 G + (0..3) (the pairing of the header)
+  __device__ static u32x4 col8(uint32_t base, int r0, int cb, int lane) {
+    const int g = lane >> 4, j = lane & 15;
+    const int col = cb + 16 * (g & 1) + 4 * (j & 3);
+    const int r = r0 + 4 * (g >> 1) + (j >> 2);
+    const uint32_t inchunk = (col & 7) << 1;
+    const u32x2 lo = ds_read_tr(base + off(r, col >> 3) + inchunk);
+    const u32x2 hi = ds_read_tr(base + off(r + 8, col >> 3) + inchunk);
+    return join(lo, hi);
+  }
+  // DMA rows [0, ROWS) of a global [token][*] block (row stride ld elements);
+  // rows >= rvalid repeat row rvalid - 1 (their products are masked).
+  template <int ROWS, int NTH>
+  __device__ static void dma(const uint16_t* G, long ld, int rvalid, uint16_t* lds) {
+    constexpr int CH = ROWS * CPR / NTH;
+    static_assert(CH * NTH == ROWS * CPR, "uneven tile DMA");
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int r = rb * 4 + kk;
-      x[kk] = r < rvalid ? *(const uint4*)(G + (long)r * ld + cb * 8) : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
-      const uint32_t p0 = __builtin_amdgcn_perm(word_of(x[1], e >> 1), word_of(x[0], e >> 1), sel);
-      const uint32_t p1 = __builtin_amdgcn_perm(word_of(x[3], e >> 1), word_of(x[2], e >> 1), sel);
-      *(uint2*)(lds + (cb * 8 + e) * LDR + rb * 4) = make_uint2(p0, p1);
+    for (int i = 0; i < CH; ++i) {
+      const int s = i * NTH + w * 64 + lane;
+      const int r = s / CPR, phys = s % CPR;
+      const int c = phys ^ f(r);
+      const int gr = min(r, rvalid - 1);
+      dma16(G + (long)gr * ld + c * 8, lds + (i * NTH + w * 64) * 8);
     }
   }
-}
+};
 
 // ------------------------------------------------------------------ forward
 
 template <int D, int NW>
 __global__ __launch_bounds__(64 * NW) void attn_fwd_mfma(AttnArgs a) {
-  constexpr int NTH = 64 * NW, BKV = 64, LDK = D + 8, LDV = BKV + 8, KS = D / 16, JB = D / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[BKV * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * LDV];
+  using T = Tile<D>;
+  constexpr int NTH = 64 * NW, BKV = 64, KS = D / 16, JB = D / 32, ST = 2;
+  constexpr int TILE = BKV * D, STAGE = 2 * TILE;       // elements: K then V
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   const int h = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int G = lane >> 5, c = lane & 31, H = a.H;
   const int q_lo = a.l + blockIdx.x * 32 * NW;       // first query of the block
@@ -132,13 +127,13 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_mfma(AttnArgs a) {
   const uint16_t* Q = (const uint16_t*)a.q;
   const uint16_t* Kc = (const uint16_t*)a.kc + h * D;
   const uint16_t* Vc = (const uint16_t*)a.vc + h * D;
+  const uint32_t sbase = lds_addr(smem);
 
-  bf16x8_t qf[KS];
+  u32x4 qf[KS];
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) {
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (tvalid) v = *(const uint4*)(Q + (long)(t - a.l) * H + h * D + 16 * kk + 8 * G);
-    qf[kk] = __builtin_bit_cast(bf16x8_t, v);
+    qf[kk] = u32x4{0, 0, 0, 0};
+    if (tvalid) qf[kk] = *(const u32x4*)(Q + (long)(t - a.l) * H + h * D + 16 * kk + 8 * G);
   }
   const float sl2 = a.scale * LOG2E;
   float m = -INFINITY, lsum = 0.f;
@@ -146,24 +141,38 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_mfma(AttnArgs a) {
 #pragma unroll
   for (int j = 0; j < JB; ++j) o[j] = zero16();
 
-  for (int kb = 0; kb < kend_blk; kb += BKV) {
-    const int kval = min(BKV, kend_blk - kb);
-    lds_copy<BKV, D, LDK, NTH>(Ks, Kc + (long)kb * H, H, kval);
-    lds_copy_t<BKV, D, LDV, NTH>(Vt, Vc + (long)kb * H, H, kval);
-    __syncthreads();
-    if (kb < kend_w) {
+  const int nkb = (kend_blk + BKV - 1) / BKV;
+  auto issue = [&](int stage, int kb) {
+    uint16_t* st = smem + stage * STAGE;
+    const int rv = min(BKV, kend_blk - kb * BKV);
+    T::template dma<BKV, NTH>(Kc + (long)kb * BKV * H, H, rv, st);
+    T::template dma<BKV, NTH>(Vc + (long)kb * BKV * H, H, rv, st + TILE);
+  };
+  issue(0, 0);
+  for (int kb = 0; kb < nkb; ++kb) {
+    wait_vm<0>();
+    __builtin_amdgcn_s_barrier();
+    if (kb + 1 < nkb) issue((kb + 1) % ST, kb + 1);
+    const int kbase = kb * BKV;
+    if (kbase < kend_w) {
+      const uint32_t Kt = sbase + (kb % ST) * STAGE * 2, Vt = Kt + TILE * 2;
       f32x16_t p[2];
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb) {
         f32x16_t s = zero16();
-        if (kb + 32 * sb < kend_w) {
+        if (kbase + 32 * sb < kend_w) {
+          u32x4 kf[KS];
 #pragma unroll
-          for (int kk = 0; kk < KS; ++kk)
-            s = mfma(lds_read16(Ks + (32 * sb + c) * LDK + 16 * kk + 8 * G), qf[kk], s);
+          for (int kk = 0; kk < KS; ++kk) kf[kk] = T::row8(Kt, 32 * sb + c, 2 * kk + G);
+          lgkm_wait(kf[0]);
+#pragma unroll
+          for (int kk = 1; kk < KS; ++kk) lgkm_tie(kf[kk]);
+#pragma unroll
+          for (int kk = 0; kk < KS; ++kk) s = mfma(kf[kk], qf[kk], s);
         }
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int key = kb + 32 * sb + 8 * (v >> 2) + 4 * G + (v & 3);
+          const int key = kbase + 32 * sb + 8 * (v >> 2) + 4 * G + (v & 3);
           p[sb][v] = (key <= t && key < a.r) ? s[v] * sl2 : -INFINITY;
         }
       }
@@ -191,17 +200,21 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_mfma(AttnArgs a) {
         for (int v = 0; v < 16; ++v) o[j][v] *= alpha;
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb) {
-        if (kb + 32 * sb >= kend_w) break;
+        if (kbase + 32 * sb >= kend_w) break;
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-          const bf16x8_t pb = acc_half_bf16(p[sb], ks);
+          const u32x4 pb = acc_half_bf16(p[sb], ks);
+          u32x4 vf[JB];
 #pragma unroll
-          for (int j = 0; j < JB; ++j)
-            o[j] = mfma(lds_pair_read(Vt + (32 * j + c) * LDV, 32 * sb + 16 * ks, G), pb, o[j]);
+          for (int j = 0; j < JB; ++j) vf[j] = T::col8(Vt, 32 * sb + 16 * ks, 32 * j, lane);
+          lgkm_wait(vf[0]);
+#pragma unroll
+          for (int j = 1; j < JB; ++j) lgkm_tie(vf[j]);
+#pragma unroll
+          for (int j = 0; j < JB; ++j) o[j] = mfma(vf[j], pb, o[j]);
         }
       }
     }
-    __syncthreads();
   }
   if (tvalid) {
     const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
@@ -239,12 +252,11 @@ __global__ __launch_bounds__(256) void attn_bwd_rowdot(AttnArgs a) {
 
 template <int D, int NW>
 __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_mfma(AttnArgs a) {
-  constexpr int NTH = 64 * NW, BQ = 32, LDQ = D + 8, LDT = BQ + 8, KS = D / 16, JB = D / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[BQ * LDQ];
-  __shared__ __attribute__((aligned(16))) uint16_t Qt[D * LDT];
-  __shared__ __attribute__((aligned(16))) uint16_t Os[BQ * LDQ];  // dO rows
-  __shared__ __attribute__((aligned(16))) uint16_t Ot[D * LDT];   // dO transposed
-  __shared__ float lse2_s[BQ], Dd_s[BQ];
+  using T = Tile<D>;
+  constexpr int NTH = 64 * NW, BQ = 32, KS = D / 16, JB = D / 32, ST = 2;
+  constexpr int TILE = BQ * D;                           // elements
+  constexpr int STAGE = 2 * TILE + NW * 128;             // Q, dO, then per-wave [lse | D]
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   const int h = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int G = lane >> 5, c = lane & 31, H = a.H;
   const int k_lo = blockIdx.x * 32 * NW;     // first key of the block
@@ -254,17 +266,16 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_mfma(AttnArgs a) {
   const uint16_t* Vc = (const uint16_t*)a.vc + h * D;
   const uint16_t* Q = (const uint16_t*)a.q + h * D;
   const uint16_t* dO = (const uint16_t*)a.dout + h * D;
+  const uint32_t sbase = lds_addr(smem);
 
-  bf16x8_t kf[KS], vf[KS];
+  u32x4 kf[KS], vf[KS];
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) {
-    uint4 x = make_uint4(0, 0, 0, 0), y = make_uint4(0, 0, 0, 0);
+    kf[kk] = vf[kk] = u32x4{0, 0, 0, 0};
     if (s_me < a.r) {
-      x = *(const uint4*)(Kc + (long)s_me * H + 16 * kk + 8 * G);
-      y = *(const uint4*)(Vc + (long)s_me * H + 16 * kk + 8 * G);
+      kf[kk] = *(const u32x4*)(Kc + (long)s_me * H + 16 * kk + 8 * G);
+      vf[kk] = *(const u32x4*)(Vc + (long)s_me * H + 16 * kk + 8 * G);
     }
-    kf[kk] = __builtin_bit_cast(bf16x8_t, x);
-    vf[kk] = __builtin_bit_cast(bf16x8_t, y);
   }
   f32x16_t dk[JB], dv[JB];
 #pragma unroll
@@ -273,26 +284,58 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_mfma(AttnArgs a) {
   const int n = a.r - a.l;
   // query rows i = t - l that can see a key of this block: t >= k_lo
   const int i_begin = max(0, k_lo - a.l) & ~(BQ - 1);
-  for (int i0 = i_begin; i0 < n; i0 += BQ) {
-    const int qval = min(BQ, n - i0);
-    lds_copy<BQ, D, LDQ, NTH>(Qs, Q + (long)i0 * H, H, qval);
-    lds_copy_t<BQ, D, LDT, NTH>(Qt, Q + (long)i0 * H, H, qval);
-    lds_copy<BQ, D, LDQ, NTH>(Os, dO + (long)i0 * H, H, qval);
-    lds_copy_t<BQ, D, LDT, NTH>(Ot, dO + (long)i0 * H, H, qval);
-    if (threadIdx.x < BQ) {
-      const int tq = a.l + i0 + threadIdx.x;
-      const bool ok = threadIdx.x < qval;
-      lse2_s[threadIdx.x] = ok ? a.lse[(long)h * a.Lmax + tq] * LOG2E : 0.f;
-      Dd_s[threadIdx.x] = ok ? a.D[(long)h * a.Lmax + tq] : 0.f;
-    }
-    __syncthreads();
+  const int nqb = (n - i_begin + BQ - 1) / BQ;
+  const float* lse_h = a.lse + (long)h * a.Lmax;
+  const float* D_h = a.D + (long)h * a.Lmax;
+  auto issue = [&](int stage, int qb) {
+    uint16_t* st = smem + stage * STAGE;
+    const int i0 = i_begin + qb * BQ, qv = min(BQ, n - i0);
+    T::template dma<BQ, NTH>(Q + (long)i0 * H, H, qv, st);
+    T::template dma<BQ, NTH>(dO + (long)i0 * H, H, qv, st + TILE);
+    // per-wave copy of lse (lanes 0..31) and D (lanes 32..63) of the block's queries
+    const int tq = min(a.l + i0 + (lane & 31), a.Lmax - 1);
+    dma4((lane < 32 ? lse_h : D_h) + tq, st + 2 * TILE + w * 128);
+  };
+  if (nqb > 0) issue(0, 0);
+  for (int qb = 0; qb < nqb; ++qb) {
+    wait_vm<0>();
+    __builtin_amdgcn_s_barrier();
+    if (qb + 1 < nqb) issue((qb + 1) % ST, qb + 1);
+    const int i0 = i_begin + qb * BQ, qval = min(BQ, n - i0);
     // the wave's keys [s_w, s_w + 32) meet queries up to l + i0 + qval - 1
     if (s_w <= a.l + i0 + qval - 1 && s_w < a.r) {
-      f32x16_t s = zero16(), dp = zero16();
+      const uint32_t Qt = sbase + (qb % ST) * STAGE * 2, Ot = Qt + TILE * 2;
+      // lse and D of this lane's 16 query rows: 4 consecutive rows per v / 4
+      const uint32_t LD = Qt + 2 * TILE * 2 + w * 256;
+      u32x4 lq[4], dq4[4];
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) {
-        s = mfma(lds_read16(Qs + c * LDQ + 16 * kk + 8 * G), kf[kk], s);
-        dp = mfma(lds_read16(Os + c * LDQ + 16 * kk + 8 * G), vf[kk], dp);
+      for (int b = 0; b < 4; ++b) {
+        lq[b] = ds_read128(LD + (8 * b + 4 * G) * 4);
+        dq4[b] = ds_read128(LD + 128 + (8 * b + 4 * G) * 4);
+      }
+      f32x16_t s = zero16(), dp = zero16();
+      {
+        u32x4 qa[KS], oa[KS];
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) {
+          qa[kk] = T::row8(Qt, c, 2 * kk + G);
+          oa[kk] = T::row8(Ot, c, 2 * kk + G);
+        }
+        lgkm_wait(qa[0]);
+#pragma unroll
+        for (int kk = 1; kk < KS; ++kk) lgkm_tie(qa[kk]);
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) lgkm_tie(oa[kk]);
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          lgkm_tie(lq[b]);
+          lgkm_tie(dq4[b]);
+        }
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) {
+          s = mfma(qa[kk], kf[kk], s);
+          dp = mfma(oa[kk], vf[kk], dp);
+        }
       }
       // s[v], dp[v]: query row qi = 8 (v / 4) + 4 G + v % 4 of the block, key s_me
       f32x16_t p, ds;
@@ -301,44 +344,94 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_mfma(AttnArgs a) {
         const int qi = 8 * (v >> 2) + 4 * G + (v & 3);
         const int tq = a.l + i0 + qi;
         const bool ok = qi < qval && s_me <= tq;
-        const float pv = ok ? exp2f(s[v] * sl2 - lse2_s[qi]) : 0.f;
+        const float lse_q = __uint_as_float(lq[v >> 2][v & 3]);
+        const float D_q = __uint_as_float(dq4[v >> 2][v & 3]);
+        const float pv = ok ? exp2f(s[v] * sl2 - lse_q * LOG2E) : 0.f;
         p[v] = pv;
-        ds[v] = pv * (dp[v] - Dd_s[qi]);
+        ds[v] = pv * (dp[v] - D_q);
       }
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-        const bf16x8_t pb = acc_half_bf16(p, ks), db = acc_half_bf16(ds, ks);
+        const u32x4 pb = acc_half_bf16(p, ks), db = acc_half_bf16(ds, ks);
+        u32x4 ob[JB], qb2[JB];
 #pragma unroll
         for (int j = 0; j < JB; ++j) {
-          dv[j] = mfma(pb, lds_pair_read(Ot + (32 * j + c) * LDT, 16 * ks, G), dv[j]);
-          dk[j] = mfma(db, lds_pair_read(Qt + (32 * j + c) * LDT, 16 * ks, G), dk[j]);
+          ob[j] = T::col8(Ot, 16 * ks, 32 * j, lane);
+          qb2[j] = T::col8(Qt, 16 * ks, 32 * j, lane);
+        }
+        lgkm_wait(ob[0]);
+#pragma unroll
+        for (int j = 1; j < JB; ++j) lgkm_tie(ob[j]);
+#pragma unroll
+        for (int j = 0; j < JB; ++j) lgkm_tie(qb2[j]);
+#pragma unroll
+        for (int j = 0; j < JB; ++j) {
+          dv[j] = mfma(pb, ob[j], dv[j]);
+          dk[j] = mfma(db, qb2[j], dk[j]);
         }
       }
     }
-    __syncthreads();
   }
-  // dk[j][v], dv[j][v]: key s_w + 8 (v / 4) + 4 G + v % 4, column 32 j + c
-#pragma unroll
-  for (int j = 0; j < JB; ++j)
+  // dk[j][v], dv[j][v]: key s_w + 8 (v / 4) + 4 G + v % 4, column 32 j + c.
+  // Added into the fp32 buffers; when all 32 keys of the wave exist, the loads
+  // of column block j + 1 are issued before block j is added and stored, so the
+  // read latency is paid about once.
+  if (s_w + 32 <= a.r) {
+    float* dkb = a.dk + (long)s_w * H + h * D + c;
+    float* dvb = a.dv + (long)s_w * H + h * D + c;
+    auto rowoff = [&](int v) { return (long)(8 * (v >> 2) + 4 * G + (v & 3)) * H; };
+    float ck[16], cv[16];
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const int key = s_w + 8 * (v >> 2) + 4 * G + (v & 3);
-      if (key < a.r) {
-        const long off = (long)key * H + h * D + 32 * j + c;
-        a.dk[off] += dk[j][v] * a.scale;
-        a.dv[off] += dv[j][v];
+      ck[v] = dkb[rowoff(v)];
+      cv[v] = dvb[rowoff(v)];
+    }
+#pragma unroll
+    for (int j = 0; j < JB; ++j) {
+      float nk[16], nv[16];
+      if (j + 1 < JB) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          nk[v] = dkb[rowoff(v) + 32 * (j + 1)];
+          nv[v] = dvb[rowoff(v) + 32 * (j + 1)];
+        }
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        dkb[rowoff(v) + 32 * j] = ck[v] + dk[j][v] * a.scale;
+        dvb[rowoff(v) + 32 * j] = cv[v] + dv[j][v];
+      }
+      if (j + 1 < JB) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          ck[v] = nk[v];
+          cv[v] = nv[v];
+        }
       }
     }
+  } else {
+#pragma unroll
+    for (int j = 0; j < JB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int key = s_w + 8 * (v >> 2) + 4 * G + (v & 3);
+        if (key < a.r) {
+          const long off = (long)key * H + h * D + 32 * j + c;
+          a.dk[off] += dk[j][v] * a.scale;
+          a.dv[off] += dv[j][v];
+        }
+      }
+  }
 }
 
 // ------------------------------------------------------------------- dQ
 
 template <int D, int NW>
 __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_mfma(AttnArgs a) {
-  constexpr int NTH = 64 * NW, BKV = 64, LDK = D + 8, LDT = BKV + 8, KS = D / 16, JB = D / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[BKV * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Kt[D * LDT];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[BKV * LDK];
+  using T = Tile<D>;
+  constexpr int NTH = 64 * NW, BKV = 64, KS = D / 16, JB = D / 32, ST = 2;
+  constexpr int TILE = BKV * D, STAGE = 2 * TILE;  // K then V
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   const int h = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int G = lane >> 5, c = lane & 31, H = a.H;
   const int q_lo = a.l + blockIdx.x * 32 * NW;
@@ -348,18 +441,17 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_mfma(AttnArgs a) {
   const int kend_w = min(a.r, q_lo + 32 * w + 32);
   const uint16_t* Kc = (const uint16_t*)a.kc + h * D;
   const uint16_t* Vc = (const uint16_t*)a.vc + h * D;
+  const uint32_t sbase = lds_addr(smem);
 
-  bf16x8_t qf[KS], of[KS];
+  u32x4 qf[KS], of[KS];
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) {
-    uint4 x = make_uint4(0, 0, 0, 0), y = make_uint4(0, 0, 0, 0);
+    qf[kk] = of[kk] = u32x4{0, 0, 0, 0};
     if (tvalid) {
       const long off = (long)(t - a.l) * H + h * D + 16 * kk + 8 * G;
-      x = *(const uint4*)((const uint16_t*)a.q + off);
-      y = *(const uint4*)((const uint16_t*)a.dout + off);
+      qf[kk] = *(const u32x4*)((const uint16_t*)a.q + off);
+      of[kk] = *(const u32x4*)((const uint16_t*)a.dout + off);
     }
-    qf[kk] = __builtin_bit_cast(bf16x8_t, x);
-    of[kk] = __builtin_bit_cast(bf16x8_t, y);
   }
   const float sl2 = a.scale * LOG2E;
   const float lse2 = tvalid ? a.lse[(long)h * a.Lmax + t] * LOG2E : 0.f;
@@ -368,38 +460,63 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_mfma(AttnArgs a) {
 #pragma unroll
   for (int j = 0; j < JB; ++j) dq[j] = zero16();
 
-  for (int kb = 0; kb < kend_blk; kb += BKV) {
-    const int kval = min(BKV, kend_blk - kb);
-    lds_copy<BKV, D, LDK, NTH>(Ks, Kc + (long)kb * H, H, kval);
-    lds_copy_t<BKV, D, LDT, NTH>(Kt, Kc + (long)kb * H, H, kval);
-    lds_copy<BKV, D, LDK, NTH>(Vs, Vc + (long)kb * H, H, kval);
-    __syncthreads();
+  const int nkb = (kend_blk + BKV - 1) / BKV;
+  auto issue = [&](int stage, int kb) {
+    uint16_t* st = smem + stage * STAGE;
+    const int rv = min(BKV, kend_blk - kb * BKV);
+    T::template dma<BKV, NTH>(Kc + (long)kb * BKV * H, H, rv, st);
+    T::template dma<BKV, NTH>(Vc + (long)kb * BKV * H, H, rv, st + TILE);
+  };
+  issue(0, 0);
+  for (int kb = 0; kb < nkb; ++kb) {
+    wait_vm<0>();
+    __builtin_amdgcn_s_barrier();
+    if (kb + 1 < nkb) issue((kb + 1) % ST, kb + 1);
+    const int kbase = kb * BKV;
+    const uint32_t Kt = sbase + (kb % ST) * STAGE * 2, Vt = Kt + TILE * 2;
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb) {
-      if (kb + 32 * sb >= kend_w) break;
+      if (kbase + 32 * sb >= kend_w) break;
       f32x16_t s = zero16(), dp = zero16();
+      {
+        u32x4 ka[KS], va[KS];
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) {
-        s = mfma(lds_read16(Ks + (32 * sb + c) * LDK + 16 * kk + 8 * G), qf[kk], s);
-        dp = mfma(lds_read16(Vs + (32 * sb + c) * LDK + 16 * kk + 8 * G), of[kk], dp);
+        for (int kk = 0; kk < KS; ++kk) {
+          ka[kk] = T::row8(Kt, 32 * sb + c, 2 * kk + G);
+          va[kk] = T::row8(Vt, 32 * sb + c, 2 * kk + G);
+        }
+        lgkm_wait(ka[0]);
+#pragma unroll
+        for (int kk = 1; kk < KS; ++kk) lgkm_tie(ka[kk]);
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) lgkm_tie(va[kk]);
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) {
+          s = mfma(ka[kk], qf[kk], s);
+          dp = mfma(va[kk], of[kk], dp);
+        }
       }
       f32x16_t ds;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int key = kb + 32 * sb + 8 * (v >> 2) + 4 * G + (v & 3);
+        const int key = kbase + 32 * sb + 8 * (v >> 2) + 4 * G + (v & 3);
         const bool ok = tvalid && key <= t;
         const float pv = ok ? exp2f(s[v] * sl2 - lse2) : 0.f;
         ds[v] = pv * (dp[v] - Dt);
       }
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-        const bf16x8_t db = acc_half_bf16(ds, ks);
+        const u32x4 db = acc_half_bf16(ds, ks);
+        u32x4 kt[JB];
 #pragma unroll
-        for (int j = 0; j < JB; ++j)
-          dq[j] = mfma(lds_pair_read(Kt + (32 * j + c) * LDT, 32 * sb + 16 * ks, G), db, dq[j]);
+        for (int j = 0; j < JB; ++j) kt[j] = T::col8(Kt, 32 * sb + 16 * ks, 32 * j, lane);
+        lgkm_wait(kt[0]);
+#pragma unroll
+        for (int j = 1; j < JB; ++j) lgkm_tie(kt[j]);
+#pragma unroll
+        for (int j = 0; j < JB; ++j) dq[j] = mfma(kt[j], db, dq[j]);
       }
     }
-    __syncthreads();
   }
   if (tvalid) {
     uint16_t* dQ = (uint16_t*)a.dq + (long)(t - a.l) * a.ld_dq + h * D;
@@ -417,11 +534,20 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_mfma(AttnArgs a) {
 
 constexpr int NWF = 4;  // waves per block
 
+template <typename K>
+hipError_t set_lds(K* fn, size_t bytes) {
+  if (bytes <= 64 * 1024) return hipSuccess;
+  return hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             (int)bytes);
+}
+
 template <int D>
 hipError_t fwd_d(const AttnArgs& a, hipStream_t s) {
   const int n = a.r - a.l;
-  dim3 grid(cdiv(n, 32 * NWF), a.heads);
-  attn_fwd_mfma<D, NWF><<<grid, 64 * NWF, 0, s>>>(a);
+  constexpr size_t lds = 2 * 2 * 64 * D * 2;
+  hipError_t e = set_lds(attn_fwd_mfma<D, NWF>, lds);
+  if (e != hipSuccess) return e;
+  attn_fwd_mfma<D, NWF><<<dim3(cdiv(n, 32 * NWF), a.heads), 64 * NWF, lds, s>>>(a);
   return hipGetLastError();
 }
 
@@ -431,10 +557,16 @@ hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
   attn_bwd_rowdot<D><<<cdiv((long)n * a.heads, 4), 256, 0, s>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  attn_bwd_dkdv_mfma<D, NWF><<<dim3(cdiv(a.r, 32 * NWF), a.heads), 64 * NWF, 0, s>>>(a);
+  constexpr size_t lds_kv = 2 * (2 * 32 * D + NWF * 128) * 2;
+  e = set_lds(attn_bwd_dkdv_mfma<D, NWF>, lds_kv);
+  if (e != hipSuccess) return e;
+  attn_bwd_dkdv_mfma<D, NWF><<<dim3(cdiv(a.r, 32 * NWF), a.heads), 64 * NWF, lds_kv, s>>>(a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  attn_bwd_dq_mfma<D, NWF><<<dim3(cdiv(n, 32 * NWF), a.heads), 64 * NWF, 0, s>>>(a);
+  constexpr size_t lds_q = 2 * 2 * 64 * D * 2;
+  e = set_lds(attn_bwd_dq_mfma<D, NWF>, lds_q);
+  if (e != hipSuccess) return e;
+  attn_bwd_dq_mfma<D, NWF><<<dim3(cdiv(n, 32 * NWF), a.heads), 64 * NWF, lds_q, s>>>(a);
   return hipGetLastError();
 }
 

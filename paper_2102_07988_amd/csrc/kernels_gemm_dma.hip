@@ -274,35 +274,50 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
     float* out = SPLIT ? a.ws + (long)blockIdx.z * a.M * a.N : (float*)a.C;
     const long ldo = SPLIT ? a.N : a.ldc;
     const int pr = lane >> 1, pc = (lane & 1) * 16;
+    const bool full = m0 + wm0 + WM <= a.M && n0 + wn0 + WN <= a.N;
+    auto dst_of = [&](int t) {
+      return out + (long)(m0 + wm0 + (t / FN) * 32 + pr) * ldo + n0 + wn0 + (t % FN) * 32 + pc;
+    };
+    float4 cur[4], nxt[4];
+    if (!SPLIT && full) {
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+      for (int q = 0; q < 4; ++q) cur[q] = *(const float4*)(dst_of(0) + 4 * q);
+    }
 #pragma unroll
-      for (int j = 0; j < FN; ++j) {
+    for (int t = 0; t < FM * FN; ++t) {
+      const int i = t / FN, j = t % FN;
+      // the next sub-tile's destination values are requested before this
+      // sub-tile is combined, so the read latency is paid about once
+      if (!SPLIT && full && t + 1 < FM * FN) {
 #pragma unroll
-        for (int v = 0; v < 16; ++v)
-          patch[(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * 36 + (lane & 31)] = acc[i][j][v];
-        const int m = m0 + wm0 + i * 32 + pr;
-        const int n = n0 + wn0 + j * 32 + pc;
-        float4 x[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) x[q] = *(const float4*)(patch + pr * 36 + pc + 4 * q);
-        if (m < a.M) {
-          float* dst = out + (long)m * ldo + n;
-          if (n + 16 <= a.N) {
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              if constexpr (!SPLIT) {
-                const float4 o = *(const float4*)(dst + 4 * q);
-                x[q].x += o.x, x[q].y += o.y, x[q].z += o.z, x[q].w += o.w;
-              }
-              *(float4*)(dst + 4 * q) = x[q];
-            }
-          } else {
-            const float* xs = (const float*)x;
-            for (int e = 0; e < 16 && n + e < a.N; ++e) dst[e] = SPLIT ? xs[e] : dst[e] + xs[e];
-          }
-        }
+        for (int q = 0; q < 4; ++q) nxt[q] = *(const float4*)(dst_of(t + 1) + 4 * q);
       }
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        patch[(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * 36 + (lane & 31)] = acc[i][j][v];
+      float4 x[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) x[q] = *(const float4*)(patch + pr * 36 + pc + 4 * q);
+      const int m = m0 + wm0 + i * 32 + pr;
+      const int n = n0 + wn0 + j * 32 + pc;
+      float* dst = out + (long)m * ldo + n;
+      if (full) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if constexpr (!SPLIT) {
+            x[q].x += cur[q].x, x[q].y += cur[q].y, x[q].z += cur[q].z, x[q].w += cur[q].w;
+          }
+          *(float4*)(dst + 4 * q) = x[q];
+        }
+      } else if (m < a.M) {
+        const float* xs = (const float*)x;
+        for (int e = 0; e < 16 && n + e < a.N; ++e) dst[e] = SPLIT ? xs[e] : dst[e] + xs[e];
+      }
+      if (!SPLIT && full && t + 1 < FM * FN) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) cur[q] = nxt[q];
+      }
+    }
   } else {
 #pragma unroll
     for (int i = 0; i < FM; ++i)

@@ -102,3 +102,37 @@ def test_long_prefix_short_slices():
     """Late slices attend to a long cached prefix (context >> slice length)."""
     _case(1, 512, 4, 520, "bf16", [384, 16, 48, 72], [8, 512], seeds=(21, 22, 23),
           label="long prefix")
+
+
+def test_profiler_table_and_dp_match_oracle():
+    """Measured cost table: -1 exactly where len + ctx > max_seq, positive
+    elsewhere; the C-ABI DP on the measured table gives exactly the oracle DP's
+    slicing and latency."""
+    from paper_2102_07988_amd import terapipe as tp
+    from oracle import dp_optimal_slicing as oracle_dp
+    H, heads, L, unit = 256, 2, 256, 32
+    params, x, dy = make_inputs(2, H, L, "bf16", (1, 2, 3))
+    dparams = [{k: v.cuda() for k, v in p.items()} for p in params]
+    for wgrad in ("per_slice", "deferred"):
+        st = tp.Stage(dparams, H, heads, L, dtype="bf16", wgrad=wgrad)
+        U = L // unit
+        lens = [unit * k for k in range(1, U + 1)]
+        ctxs = [unit * j for j in range(U)]
+        tf, tb = st.profile(lens, ctxs, warmup=1, reps=3)
+        for i in range(U):
+            for j in range(U):
+                if lens[i] + ctxs[j] > L:
+                    assert tf[i, j] == -1 and tb[i, j] == -1
+                else:
+                    assert tf[i, j] > 0 and tb[i, j] > 0
+        cost = np.where(tf >= 0, tf + tb, -1).astype(np.int64)
+        for K in (1, 4, 48):
+            units, T, _, _ = oracle_dp(cost, K)
+            got, T2 = tp.dp_optimal_slicing(cost, unit, K)
+            assert T2 == T and got == [unit * u for u in units], (wgrad, K)
+        # the stage is usable again after profiling
+        st.zero_grads()
+        y, dx = st.run_sequence(x.cuda(), dy.cuda(), [128, 128])
+        torch.cuda.synchronize()
+        assert torch.isfinite(y.float()).all() and torch.isfinite(dx.float()).all()
+        del st
