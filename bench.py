@@ -42,7 +42,7 @@ PEAK_HBM_GBS = 8000.0
 TRAFFIC = {
     "gemm_bwd_dw_tn": {"workload": "gpt3-175b-stage",
                        "source": "paper_2102_07988_amd/csrc/kernels_gemm_dma.hip",
-                       "sha256_16": "6dedf2a5be3411d1", "bytes_per_launch": 9712414292},
+                       "sha256_16": "1c639cb26967c295", "bytes_per_launch": 7990755824},
 }
 
 

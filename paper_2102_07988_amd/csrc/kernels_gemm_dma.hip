@@ -173,6 +173,30 @@ __device__ inline void wait_tiles(int pending) {
   }
 }
 
+// XCD-aware output-tile order for launches of many tiles.  Workgroups are
+// dispatched round-robin over the 8 XCDs (workgroup g runs on XCD g % 8) and
+// each CU holds one workgroup, so the j-th workgroup of an XCD belongs to
+// "round" j / 32 of that XCD's 32 CUs.  The 32 workgroups of one XCD and
+// round cover a 4 x 8 super-tile of output tiles, so each k-slice of its 4
+// A-panels and 8 B-panels is fetched into that XCD's L2 once while they run
+// side by side.  Super-tile s of round r is r * 8 + xcd.
+constexpr int WALK_PER_XCD = 32;
+
+struct TileWalk {
+  static constexpr int SM = 4, SN = 8;
+  int tm, tn, stm, stn;
+  __device__ TileWalk(int tiles_m, int tiles_n)
+      : tm(tiles_m), tn(tiles_n), stm((tiles_m + SM - 1) / SM), stn((tiles_n + SN - 1) / SN) {}
+  // output tile of workgroup (xcd, slot) in round r; -1 if that slot is idle
+  __device__ int tile(int r, int xcd, int slot) const {
+    const int s = r * 8 + xcd;
+    if (s >= stm * stn) return -1;
+    const int im = (s / stn) * SM + slot / SN, in = (s % stn) * SN + slot % SN;
+    if (im >= tm || in >= tn) return -1;
+    return im * tn + in;
+  }
+};
+
 template <int BM, int BN, int BK, int WGM, int WGN, bool A_KC, bool B_KC, int EPI, bool SPLIT,
           int STAGES>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
@@ -189,13 +213,22 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
   const uint16_t* B = (const uint16_t*)a.B;
   const long lda = A_KC ? a.sam : a.sak;
   const long ldb = B_KC ? a.sbn : a.sbk;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm0 = (wave / WGN) * WM, wn0 = (wave % WGN) * WN;
   const int kbeg = SPLIT ? blockIdx.z * a.k_split : 0;
   const int kend = SPLIT ? min(a.K, kbeg + a.k_split) : a.K;
   const int nk = (kend - kbeg) / BK;
   const uint32_t sbase = lds_addr(smem);
+
+  int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  if (!SPLIT && a.walk) {
+    const TileWalk walk(cdiv(a.M, BM), cdiv(a.N, BN));
+    const int j = blockIdx.x / 8;
+    const int tile = walk.tile(j / WALK_PER_XCD, blockIdx.x % 8, j % WALK_PER_XCD);
+    if (tile < 0) return;  // uniform per workgroup
+    m0 = (tile / walk.tn) * BM;
+    n0 = (tile % walk.tn) * BN;
+  }
 
   auto issue = [&](int stage, int kt) {
     uint16_t* st = smem + stage * STAGE;
@@ -337,6 +370,12 @@ hipError_t launch_dma(const GemmArgs& a, hipStream_t s) {
   constexpr int NTH = 64 * WGM * WGN;
   constexpr size_t lds = (size_t)STAGES * (BM + BN) * BK * 2;
   dim3 grid(cdiv(a.N, BN), cdiv(a.M, BM), SPLIT ? a.splits : 1);
+  if (!SPLIT && a.walk) {
+    // rounds of 8 super-tiles (one per XCD), 256 workgroups per round
+    const int rounds =
+        (cdiv(cdiv(a.M, BM), TileWalk::SM) * cdiv(cdiv(a.N, BN), TileWalk::SN) + 7) / 8;
+    grid = dim3(rounds * 8 * WALK_PER_XCD, 1, 1);
+  }
 #define TP_LAUNCH(E)                                                                         \
   do {                                                                                       \
     auto* fn = gemm_dma_kernel<BM, BN, BK, WGM, WGN, A_KC, B_KC, E, SPLIT, STAGES>;        \
@@ -401,6 +440,8 @@ hipError_t run_dma(GemmArgs a, hipStream_t s) {
     if (e != hipSuccess) return e;
     return gemm_splitk_reduce(a, s);
   }
+  // many tiles: XCD-aware super-tile order
+  if (tiles >= 2 * CUS) a.walk = 1;
   return launch_dma<BM, BN, BK, WGM, WGN, A_KC, B_KC, STAGES, false>(a, s);
 }
 
@@ -426,6 +467,8 @@ hipError_t gemm_dma_bf16_cfg(int cfg, const GemmArgs& a, hipStream_t s) {
   if (((uintptr_t)a.A & 15) || ((uintptr_t)a.B & 15)) return hipErrorNotSupported;
   const long lda = a_kc ? a.sam : a.sak, ldb = b_kc ? a.sbn : a.sbk;
   if ((lda & 7) || (ldb & 7)) return hipErrorNotSupported;
+  // fp32 outputs leave as 16-byte row segments
+  if (a.epi == EPI_ACC_F32 && (((uintptr_t)a.C & 15) || (a.ldc & 3))) return hipErrorNotSupported;
   if (cfg < 0) {
     // measured on the stage shapes: 256 x 256 tiles (2 stages) everywhere except
     // small row counts and wide forward outputs, which prefer 256 x 128 (3 stages)

@@ -103,6 +103,6 @@ __device__ inline float block_max(float v, float* red) {
   return s;
 }
 
-inline int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
+__host__ __device__ inline int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
 
 }  // namespace tp

@@ -42,6 +42,8 @@ struct GemmArgs {
   long ws_elems = 0;
   // set by the launcher: reduction range of one split and the split count
   int k_split = 0, splits = 1;
+  // set by the launcher: output-tile order (0 grid order, 1 XCD super-tiles)
+  int walk = 0;
 };
 
 hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s);
