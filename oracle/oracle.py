@@ -11,6 +11,9 @@ pieces that need no speed:
 * ``slice_flops`` / ``paper_tflops_per_gpu`` -- the arithmetic a slice of a
   pre-LN block must do, and the per-GPU TFLOP/s convention of the paper's
   result tables (Tables 2-4 in the appendix).
+* ``fit_ctx_model`` / ``cost_table_from_model`` -- the cost estimate of
+  Sec. 3.3 (Eq. 9): t(i, j) = t(i, 0) + t_ctx(i, j) with the context overhead
+  t_ctx = a0 + a1 i + a2 j + a3 i j fitted by least squares.
 """
 from __future__ import annotations
 
@@ -264,3 +267,47 @@ def paper_tflops_per_gpu(hidden: int, n_layers: int, seq_len: int, sequences: in
     of one data-parallel replica, divided by all GPUs and the iteration time."""
     per_token_layer = 72 * hidden * hidden + 6 * hidden * seq_len
     return per_token_layer * n_layers * seq_len * sequences / (gpus * latency_s) / 1e12
+
+
+# ------------------------------------------------------- cost model (Eq. 9)
+
+def fit_ctx_model(t0: Sequence[int], unit: int, samples: Sequence[Tuple[int, int, int]]):
+    """Least-squares fit of the context overhead of Eq. 9.
+
+    ``t0[k-1]`` is the measured cost of a slice of k*unit tokens with no
+    context; each sample (i, j, t) is a measured cost t of a slice of i tokens
+    (a multiple of ``unit``) after j > 0 tokens of context, whose overhead is
+    t - t(i, 0).  Returns (a0, a1, a2, a3) minimising the sum of squared
+    differences between that overhead and a0 + a1 i + a2 j + a3 i j, i and j
+    in tokens, the definition of least squares solved by numpy's lstsq on the
+    unscaled design in float64."""
+    X = np.array([[1.0, float(i), float(j), float(i) * float(j)] for i, j, _ in samples])
+    y = np.array([float(t) - float(t0[i // unit - 1]) for i, j, t in samples])
+    coef, _, rank, _ = np.linalg.lstsq(X, y, rcond=None)
+    if rank < 4:
+        raise ValueError("samples do not determine the four coefficients")
+    return tuple(float(c) for c in coef)
+
+
+def _round_half_away(x: float) -> int:
+    return int(math.floor(x + 0.5)) if x >= 0 else -int(math.floor(-x + 0.5))
+
+
+def cost_table_from_model(t0: Sequence[int], unit: int, coef) -> np.ndarray:
+    """[U][U] int64 cost table from Eq. 9: entry [k-1, j] is t(k units, j units
+    of context) = t(k units, 0) measured, plus, for j > 0, the fitted overhead
+    a0 + a1 i + a2 c + a3 i c at i = k*unit, c = j*unit tokens, rounded to the
+    nearest nanosecond (halves away from zero) and the sum clamped at 0.
+    Entries past the sequence (k + j > U) are -1."""
+    U = len(t0)
+    a0, a1, a2, a3 = coef
+    cost = np.full((U, U), -1, dtype=np.int64)
+    for k in range(1, U + 1):
+        for j in range(0, U - k + 1):
+            if j == 0:
+                cost[k - 1, j] = int(t0[k - 1])
+            else:
+                i, c = k * unit, j * unit
+                pred = a0 + a1 * i + a2 * c + a3 * i * c
+                cost[k - 1, j] = max(0, int(t0[k - 1]) + _round_half_away(pred))
+    return cost
