@@ -96,12 +96,50 @@ def cpu_baseline(params0, x, dy, hidden: int, heads: int, n_tokens: int):
                       f"{n_tokens} tokens at context 0, forward+backward, fp64"}
 
 
+def _subset(U: int):
+    """Model-mode subset in units: a few lengths x a few contexts (Sec. 3.3 fits
+    the overhead on a subset of the (i, j) grid)."""
+    ks = sorted({k for k in (1, 2, U // 8, U // 4, U // 2, 3 * U // 4) if 1 <= k < U})
+    js = sorted({j for j in (1, U // 8, U // 4, U // 2, 3 * U // 4) if 1 <= j < U})
+    return ks, js
+
+
+def _eq5(cost, units, K):
+    ts, c = [], 0
+    for u in units:
+        ts.append(int(cost[u - 1, c]))
+        c += u
+    return sum(ts) + (K - 1) * max(ts), sum(ts)
+
+
+def _slicing_summary(tp, cost, unit, K):
+    """DP slicing of a table and Eq. 5 latencies of the uniform slicings."""
+    U = cost.shape[0]
+    t1 = time.perf_counter()
+    dp_lens, dp_T = tp.dp_optimal_slicing(cost, unit, K)
+    dp_s = time.perf_counter() - t1
+    uniform = {str(m): round(_eq5(cost, [U // m] * m, K)[0] / 1e6, 3)
+               for m in range(1, U + 1) if U % m == 0}
+    best_m = min(uniform, key=uniform.get)
+    return {"dp_slicing": dp_lens, "dp_T_ms": round(dp_T / 1e6, 3), "dp_seconds": round(dp_s, 4),
+            "uniform_T_ms": uniform, "best_uniform_slices": int(best_m),
+            "dp_speedup_vs_best_uniform": round(uniform[best_m] / (dp_T / 1e6), 4),
+            "single_slice_T_ms": uniform["1"]}
+
+
 def pipeline_report(st, tp, L: int, unit: int, K: int, warmup: int, reps: int,
-                    seq_ms: float, dw_ms: float):
-    """Measure the per-slice cost table t(len, ctx) = t_fwd + t_bwd on this stage
-    (lengths and contexts in multiples of `unit`), solve the optimal slicing for a
-    pipeline of K such stages (Eq. 5-8, Algorithm 1) and compare Eq. 5 latencies
-    of the DP slicing, uniform slicings and one slice."""
+                    run_slicing, dw_ms: float, fine_unit: int, fine_K=(48, 96)):
+    """Per-slice cost tables t(len, ctx) = t_fwd + t_bwd of this stage and the
+    slicings they give for a pipeline of K such stages (Eq. 5-8, Algorithm 1):
+
+    * the full table measured at every (len, ctx) on a grid of `unit` tokens:
+      DP vs uniform vs one slice, and the DP slicing run back to back on the
+      stage against the sum of its table entries;
+    * the model-mode table (Eq. 9) on the same grid from t(i, 0) plus a fitted
+      context overhead: its prediction error on the points it did not measure
+      and the latency its DP slicing reaches on the measured table;
+    * a model-mode table on a fine grid of `fine_unit` tokens (too many points
+      to measure one by one): DP vs uniform slicings for each K in fine_K."""
     import numpy as np
 
     U = L // unit
@@ -110,38 +148,67 @@ def pipeline_report(st, tp, L: int, unit: int, K: int, warmup: int, reps: int,
     t0 = time.perf_counter()
     tf, tb = st.profile(lens, ctxs, warmup=warmup, reps=reps)
     prof_s = time.perf_counter() - t0
-    cost = np.full((U, U), -1, dtype=np.int64)
-    for k in range(U):
-        for j in range(U):
-            if k + 1 + j <= U:
-                cost[k, j] = tf[k, j] + tb[k, j]
-    t1 = time.perf_counter()
-    dp_lens, dp_T = tp.dp_optimal_slicing(cost, unit, K)
-    dp_s = time.perf_counter() - t1
+    cost = np.where(tf >= 0, tf + tb, -1).astype(np.int64)
+    rep = {"K": K, "unit": unit, "table_points": int((cost >= 0).sum()),
+           "profile_seconds": round(prof_s, 2)}
+    rep.update(_slicing_summary(tp, cost, unit, K))
+    dp_units = [n // unit for n in rep["dp_slicing"]]
+    measured_ms = run_slicing(rep["dp_slicing"])
+    table_sum = _eq5(cost, dp_units, K)[1] / 1e6
+    rep["back_to_back"] = {
+        "slicing": rep["dp_slicing"], "measured_ms": round(measured_ms, 3),
+        "measured_minus_deferred_dw_ms": round(measured_ms - dw_ms, 3),
+        "table_sum_ms": round(table_sum, 3),
+        "ratio": round((measured_ms - dw_ms) / table_sum, 4)}
 
-    def eq5(units):
-        ts, c = [], 0
-        for u in units:
-            ts.append(int(cost[u - 1, c]))
-            c += u
-        return sum(ts) + (K - 1) * max(ts)
+    # model mode on the same grid
+    ks, js = _subset(U)
+    t0 = time.perf_counter()
+    mcost, coef = st.profile_model(L, unit, [unit * k for k in ks], [unit * j for j in js],
+                                   warmup=warmup, reps=reps)
+    mprof_s = time.perf_counter() - t0
+    sub = {(k, j) for k in ks for j in js if k + j <= U}
+    ov_err, t_err = [], []
+    for k in range(1, U + 1):
+        for j in range(1, U - k + 1):
+            if (k, j) in sub:
+                continue
+            i, c = k * unit, j * unit
+            actual_ov = cost[k - 1, j] - cost[k - 1, 0]
+            pred_ov = coef[0] + coef[1] * i + coef[2] * c + coef[3] * i * c
+            if actual_ov > 0:
+                ov_err.append(abs(pred_ov - actual_ov) / actual_ov)
+            t_err.append(abs(mcost[k - 1, j] - cost[k - 1, j]) / cost[k - 1, j])
+    m_lens, _ = tp.dp_optimal_slicing(mcost, unit, K)
+    m_T = _eq5(cost, [n // unit for n in m_lens], K)[0]
+    rep["model"] = {
+        "unit": unit, "points_measured": U + len(sub), "profile_seconds": round(mprof_s, 2),
+        "coef_ns": [round(v, 6) for v in coef],
+        "heldout_points": len(t_err),
+        "heldout_overhead_rel_err_median": round(float(np.median(ov_err)), 4) if ov_err else None,
+        "heldout_overhead_rel_err_p90": round(float(np.percentile(ov_err, 90)), 4) if ov_err else None,
+        "heldout_cost_rel_err_median": round(float(np.median(t_err)), 4) if t_err else None,
+        "heldout_cost_rel_err_max": round(float(np.max(t_err)), 4) if t_err else None,
+        "dp_slicing": m_lens, "dp_T_on_measured_table_ms": round(m_T / 1e6, 3),
+        "vs_measured_table_dp": round(m_T / (rep["dp_T_ms"] * 1e6), 4)}
 
-    uniform = {}
-    for m in range(1, U + 1):
-        if U % m == 0:
-            uniform[str(m)] = round(eq5([U // m] * m) / 1e6, 3)
-    best_m = min(uniform, key=uniform.get)
-    return {
-        "K": K, "unit": unit, "table_points": int((cost >= 0).sum()),
-        "profile_seconds": round(prof_s, 2), "dp_seconds": round(dp_s, 4),
-        "dp_slicing": dp_lens, "dp_T_ms": round(dp_T / 1e6, 3),
-        "uniform_T_ms": uniform, "best_uniform_slices": int(best_m),
-        "dp_speedup_vs_best_uniform": round(uniform[best_m] / (dp_T / 1e6), 4),
-        "single_slice_T_ms": uniform["1"],
-        "deferred_dw_ms_per_sequence": round(dw_ms, 3),
-        "note": "T = Eq. 5 over the measured t_fwd + t_bwd table; in deferred mode the "
-                "once-per-sequence dW GEMMs (deferred_dw_ms) add to the last stage's tail",
-    }
+    # model mode on the fine grid
+    if fine_unit and L % fine_unit == 0 and fine_unit < unit:
+        Uf = L // fine_unit
+        ks, js = _subset(Uf)
+        t0 = time.perf_counter()
+        fcost, fcoef = st.profile_model(L, fine_unit, [fine_unit * k for k in ks],
+                                        [fine_unit * j for j in js], warmup=warmup, reps=reps)
+        fprof_s = time.perf_counter() - t0
+        rep["model_fine"] = {
+            "unit": fine_unit, "points_measured": Uf + sum(1 for k in ks for j in js if k + j <= Uf),
+            "table_points": int((fcost >= 0).sum()), "profile_seconds": round(fprof_s, 2),
+            "coef_ns": [round(v, 6) for v in fcoef],
+            "by_K": {str(k): _slicing_summary(tp, fcost, fine_unit, k) for k in fine_K}}
+    rep["deferred_dw_ms_per_sequence"] = round(dw_ms, 3)
+    rep["note"] = ("T = Eq. 5 over t_fwd + t_bwd tables; in deferred mode the once-per-sequence "
+                   "dW GEMMs (deferred_dw_ms) add to the last stage's tail and are not in t")
+    return rep
 
 
 def main():
@@ -159,6 +226,9 @@ def main():
                     help="skip the cost-table / DP / Eq. 5 pipeline-latency report")
     ap.add_argument("--pipeline-unit", type=int, default=128)
     ap.add_argument("--pipeline-K", type=int, default=48)
+    ap.add_argument("--pipeline-fine-unit", type=int, default=16,
+                    help="grid of the model-mode (Eq. 9) table for the uniform-vs-DP sweep; "
+                         "0 skips it")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (4 times), for "
                          "scaling the HBM byte counters")
@@ -268,8 +338,28 @@ def main():
     }
     if not args.no_pipeline:
         dw_ms = kernels.get("gemm_bwd_dw_tn", {}).get("ms_per_step", 0.0) if args.wgrad == "deferred" else 0.0
+        def run_slicing(sl):
+            b = [0]
+            for n in sl:
+                b.append(b[-1] + n)
+
+            def seq():
+                st.reset()
+                for i in range(len(sl)):
+                    st.forward(b[i], b[i + 1], x[b[i]:b[i + 1]], out=y[b[i]:b[i + 1]])
+                for i in range(len(sl) - 1, -1, -1):
+                    st.backward(b[i], b[i + 1], dy[b[i]:b[i + 1]], out=dx[b[i]:b[i + 1]])
+            seq()
+            torch.cuda.synchronize()
+            reps = 3
+            ta = time.perf_counter()
+            for _ in range(reps):
+                seq()
+            torch.cuda.synchronize()
+            return (time.perf_counter() - ta) * 1e3 / reps
+
         out["pipeline"] = pipeline_report(st, tp, L, args.pipeline_unit, args.pipeline_K, 1, 3,
-                                          ms, dw_ms)
+                                          run_slicing, dw_ms, args.pipeline_fine_unit)
         st.zero_grads()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(params[0], x, dy, H, heads, args.cpu_baseline_tokens)

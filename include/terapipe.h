@@ -159,6 +159,43 @@ tp_status tp_profile_slice_cost(tp_stage *stage, const int *lens, int n_lens, co
 tp_status tp_dp_optimal_slicing(const int64_t *cost, int L_units, int unit, int K, int64_t eps_ns,
                                 int *out_lens, int *out_M, int64_t *out_T);
 
+/* Cost estimate of Sec. 3.3 (Eq. 9): t(i, j) = t(i, 0) + t_ctx(i, j) with the
+ * context overhead t_ctx(i, j) = a0 + a1 i + a2 j + a3 i j (i = slice length,
+ * j = context length, both in tokens) fitted by least squares.
+ *
+ * tp_fit_ctx_model: t0_ns (host, [L_units]): t0_ns[k-1] = t(k*unit tokens, 0).
+ * Samples s = 0..n_samples-1 (host arrays): a slice of s_len[s] tokens (a
+ * multiple of unit) after s_ctx[s] >= 1 tokens of context cost s_t_ns[s]; its
+ * overhead is s_t_ns[s] - t0_ns[s_len[s]/unit - 1].  Writes coef[0..3] =
+ * a0 (ns), a1, a2 (ns per token), a3 (ns per token^2) minimising the sum of
+ * squared overhead residuals.  Host only, deterministic.  Errors:
+ * TP_ERR_INVALID (null pointer, n_samples < 4, a sample off the unit grid or
+ * past L_units*unit tokens, a negative time, or samples that do not determine
+ * the four coefficients, e.g. a single length or a single context). */
+tp_status tp_fit_ctx_model(const int64_t *t0_ns, int L_units, int unit, const int *s_len,
+                           const int *s_ctx, const int64_t *s_t_ns, int n_samples, double *coef);
+
+/* Cost table for tp_dp_optimal_slicing from the Eq. 9 model: cost (host,
+ * [L_units][L_units]) entry (k-1)*L_units + j = t0_ns[k-1] for j = 0, and
+ * t0_ns[k-1] + llround(a0 + a1 i + a2 c + a3 i c) at i = k*unit, c = j*unit
+ * for j > 0, clamped at 0; entries with k + j > L_units are -1.  Host only.
+ * Errors: TP_ERR_INVALID (null pointer, L_units < 1, unit < 1, negative t0). */
+tp_status tp_cost_table_from_model(const int64_t *t0_ns, int L_units, int unit, const double *coef,
+                                   int64_t *cost);
+
+/* Profile in model mode (Sec. 3.3, Eq. 9): measure t(i, 0) = t_fwd + t_bwd for
+ * every length i = unit .. L_units*unit with tp_profile_slice_cost, measure the
+ * subset sub_lens x sub_ctxs (lengths multiples of unit, contexts >= 1; pairs
+ * past L_units*unit tokens are skipped), fit the overhead model and write the
+ * [L_units][L_units] cost table (layout of tp_cost_table_from_model) and the
+ * coefficients coef[0..3].  The stage needs max_seq >= L_units*unit.
+ * Synchronous; clobbers the K/V cache, arenas and gradients like
+ * tp_profile_slice_cost.  Errors: TP_ERR_INVALID (bad arguments, fewer than 4
+ * usable subset points, a subset that does not determine the model), TP_ERR_HIP. */
+tp_status tp_profile_cost_model(tp_stage *stage, int L_units, int unit, const int *sub_lens,
+                                int n_sub_lens, const int *sub_ctxs, int n_sub_ctxs, int warmup,
+                                int reps, int64_t *cost, double *coef);
+
 /* Static description of a status code. */
 const char *tp_status_string(tp_status status);
 

@@ -29,7 +29,8 @@ SYNTH_NAMES = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
 
 EXPORTED = ("tp_stage_workspace_bytes", "tp_stage_init", "tp_stage_destroy",
             "tp_kv_prefix_reset", "tp_slice_forward", "tp_slice_backward",
-            "tp_profile_slice_cost", "tp_dp_optimal_slicing", "tp_status_string",
+            "tp_profile_slice_cost", "tp_dp_optimal_slicing", "tp_fit_ctx_model",
+            "tp_cost_table_from_model", "tp_profile_cost_model", "tp_status_string",
             "tp_stage_enable_kernel_timing", "tp_stage_kernel_stats")
 
 
@@ -80,6 +81,15 @@ def _load():
     lib.tp_dp_optimal_slicing.restype = ctypes.c_int
     lib.tp_dp_optimal_slicing.argtypes = [i64p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                           ctypes.c_int64, ip, ip, i64p]
+    dp = ctypes.POINTER(ctypes.c_double)
+    lib.tp_fit_ctx_model.restype = ctypes.c_int
+    lib.tp_fit_ctx_model.argtypes = [i64p, ctypes.c_int, ctypes.c_int, ip, ip, i64p, ctypes.c_int,
+                                     dp]
+    lib.tp_cost_table_from_model.restype = ctypes.c_int
+    lib.tp_cost_table_from_model.argtypes = [i64p, ctypes.c_int, ctypes.c_int, dp, i64p]
+    lib.tp_profile_cost_model.restype = ctypes.c_int
+    lib.tp_profile_cost_model.argtypes = [vp, ctypes.c_int, ctypes.c_int, ip, ctypes.c_int, ip,
+                                          ctypes.c_int, ctypes.c_int, ctypes.c_int, i64p, dp]
     lib.tp_status_string.restype = ctypes.c_char_p
     lib.tp_status_string.argtypes = [ctypes.c_int]
     lib.tp_stage_enable_kernel_timing.restype = ctypes.c_int
@@ -233,6 +243,24 @@ class Stage:
                "tp_profile_slice_cost")
         return tf, tb
 
+    def profile_model(self, L: int, unit: int, sub_lens: Sequence[int], sub_ctxs: Sequence[int],
+                      warmup: int = 3, reps: int = 10) -> Tuple[np.ndarray, Tuple[float, ...]]:
+        """Model-mode cost table (Eq. 9): every t(i, 0) measured, the context
+        overhead fitted on sub_lens x sub_ctxs.  Returns (int64 [U][U] table of
+        t_fwd + t_bwd in ns, (a0, a1, a2, a3))."""
+        if L % unit:
+            raise ValueError("L must be a multiple of unit")
+        U = L // unit
+        nl, nc = len(sub_lens), len(sub_ctxs)
+        Ls = (ctypes.c_int * nl)(*sub_lens)
+        Cs = (ctypes.c_int * nc)(*sub_ctxs)
+        cost = np.zeros((U, U), dtype=np.int64)
+        coef = (ctypes.c_double * 4)()
+        _check(lib.tp_profile_cost_model(self._h, U, unit, Ls, nl, Cs, nc, warmup, reps,
+                                         cost.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                                         coef), "tp_profile_cost_model")
+        return cost, tuple(coef)
+
     def enable_kernel_timing(self, on: bool = True):
         _check(lib.tp_stage_enable_kernel_timing(self._h, 1 if on else 0), "kernel timing")
 
@@ -258,6 +286,33 @@ def dp_optimal_slicing(cost: np.ndarray, unit: int, K: int, eps_ns: int = 0):
                                      K, eps_ns, out, ctypes.byref(M), ctypes.byref(T)),
            "tp_dp_optimal_slicing")
     return [out[i] for i in range(M.value)], T.value
+
+
+def fit_ctx_model(t0: Sequence[int], unit: int, samples: Sequence[Tuple[int, int, int]]):
+    """C-ABI Eq. 9 fit: t0[k-1] = t(k*unit, 0); samples (len, ctx, t) with ctx >= 1.
+    Returns (a0, a1, a2, a3) of t_ctx = a0 + a1 len + a2 ctx + a3 len ctx (ns, tokens)."""
+    U, n = len(t0), len(samples)
+    t0a = np.ascontiguousarray(t0, dtype=np.int64)
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    sl = (ctypes.c_int * n)(*[s[0] for s in samples])
+    sc = (ctypes.c_int * n)(*[s[1] for s in samples])
+    st = np.ascontiguousarray([s[2] for s in samples], dtype=np.int64)
+    coef = (ctypes.c_double * 4)()
+    _check(lib.tp_fit_ctx_model(t0a.ctypes.data_as(i64p), U, unit, sl, sc, st.ctypes.data_as(i64p),
+                                n, coef), "tp_fit_ctx_model")
+    return tuple(coef)
+
+
+def cost_table_from_model(t0: Sequence[int], unit: int, coef) -> np.ndarray:
+    """C-ABI Eq. 9 cost table, int64 [U][U] (layout of dp_optimal_slicing's input)."""
+    U = len(t0)
+    t0a = np.ascontiguousarray(t0, dtype=np.int64)
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    c = (ctypes.c_double * 4)(*coef)
+    cost = np.zeros((U, U), dtype=np.int64)
+    _check(lib.tp_cost_table_from_model(t0a.ctypes.data_as(i64p), U, unit, c,
+                                        cost.ctypes.data_as(i64p)), "tp_cost_table_from_model")
+    return cost
 
 
 def slice_flops(n: int, c: int, hidden: int) -> int:

@@ -136,3 +136,39 @@ def test_profiler_table_and_dp_match_oracle():
         torch.cuda.synchronize()
         assert torch.isfinite(y.float()).all() and torch.isfinite(dx.float()).all()
         del st
+
+
+def test_profile_cost_model_mode():
+    """Model-mode profiling (Eq. 9): the table has the measured-table layout,
+    its j = 0 column is positive, and the model's predictions at the subset
+    points it was fitted on stay close to the costs measured again there (the
+    fit is a least-squares fit to those very points, so only timing noise and
+    model error separate them)."""
+    from paper_2102_07988_amd import terapipe as tp
+    H, heads, L, unit = 512, 4, 512, 32
+    params, _, _ = make_inputs(2, H, L, "bf16", (4, 5, 6))
+    dparams = [{k: v.cuda() for k, v in p.items()} for p in params]
+    st = tp.Stage(dparams, H, heads, L, dtype="bf16", wgrad="deferred")
+    U = L // unit
+    sub_lens, sub_ctxs = [32, 128, 256, 384], [32, 128, 256, 448]
+    cost, coef = st.profile_model(L, unit, sub_lens, sub_ctxs, warmup=2, reps=5)
+    assert all(np.isfinite(coef))
+    for k in range(1, U + 1):
+        assert cost[k - 1, 0] > 0
+        for j in range(U):
+            assert (cost[k - 1, j] == -1) == (k + j > U)
+            if k + j <= U:
+                assert cost[k - 1, j] >= 0
+    # the table rebuilt from its own j = 0 column and coefficients is identical
+    assert np.array_equal(tp.cost_table_from_model(cost[:, 0], unit, coef), cost)
+    tf, tb = st.profile(sub_lens, sub_ctxs, warmup=2, reps=5)
+    errs = []
+    for a, i in enumerate(sub_lens):
+        for b, c in enumerate(sub_ctxs):
+            if i + c <= L:
+                errs.append(abs(cost[i // unit - 1, c // unit] - (tf[a, b] + tb[a, b]))
+                            / (tf[a, b] + tb[a, b]))
+    assert np.median(errs) < 0.25, errs
+    # the DP runs on the model table
+    lens, T = tp.dp_optimal_slicing(cost, unit, 8)
+    assert sum(lens) == L and T > 0
