@@ -128,7 +128,8 @@ def _slicing_summary(tp, cost, unit, K):
 
 
 def pipeline_report(st, tp, L: int, unit: int, K: int, warmup: int, reps: int,
-                    run_slicing, dw_ms: float, fine_unit: int, fine_K=(48, 96)):
+                    run_slicing, dw_ms: float, fine_unit: int, n_layers: int, H: int,
+                    deferred: bool, fine_K=(48, 96)):
     """Per-slice cost tables t(len, ctx) = t_fwd + t_bwd of this stage and the
     slicings they give for a pipeline of K such stages (Eq. 5-8, Algorithm 1):
 
@@ -151,6 +152,22 @@ def pipeline_report(st, tp, L: int, unit: int, K: int, warmup: int, reps: int,
     cost = np.where(tf >= 0, tf + tb, -1).astype(np.int64)
     rep = {"K": K, "unit": unit, "table_points": int((cost >= 0).sum()),
            "profile_seconds": round(prof_s, 2)}
+    # slice throughput vs (len, ctx): the stage's fwd + bwd flops of one slice
+    # (without the deferred once-per-sequence dW GEMMs, which the table does
+    # not time) over the measured t_fwd + t_bwd
+    pts = []
+    n = unit
+    while n <= L:
+        for c in sorted({0, L // 2 - n if L // 2 >= n else 0, L - n}):
+            if c < 0 or (c % unit):
+                continue
+            t_ns = int(cost[n // unit - 1, c // unit])
+            fl = n_layers * (tp.slice_flops(n, c, H) - (24 * n * H * H if deferred else 0))
+            pts.append({"len": n, "ctx": c, "t_ms": round(t_ns / 1e6, 3),
+                        "tflops": round(fl / (t_ns * 1e-9) / 1e12, 1),
+                        "pct_bf16_peak": round(100 * fl / (t_ns * 1e-9) / 1e12 / PEAK_BF16_TFLOPS, 1)})
+        n *= 2
+    rep["slice_tflops"] = pts
     rep.update(_slicing_summary(tp, cost, unit, K))
     dp_units = [n // unit for n in rep["dp_slicing"]]
     measured_ms = run_slicing(rep["dp_slicing"])
@@ -306,8 +323,11 @@ def main():
     kernels = {}
     if stats:
         for name, s in stats.items():
+            secs = max(s["total_ms"], 1e-9) * 1e-3
             kernels[name] = {"launches": s["launches"], "ms_per_step": s["total_ms"] / args.steps,
-                             "avg_us": 1e3 * s["total_ms"] / max(1, s["launches"])}
+                             "avg_us": 1e3 * s["total_ms"] / max(1, s["launches"]),
+                             "achieved_tflops": round(s["flops"] / secs / 1e12, 2),
+                             "achieved_gbs": round(s["bytes"] / secs / 1e9, 1)}
         dom = max(stats, key=lambda k: stats[k]["total_ms"])
         s = stats[dom]
         secs = s["total_ms"] * 1e-3
@@ -359,8 +379,10 @@ def main():
             return (time.perf_counter() - ta) * 1e3 / reps
 
         out["pipeline"] = pipeline_report(st, tp, L, args.pipeline_unit, args.pipeline_K, 1, 3,
-                                          run_slicing, dw_ms, args.pipeline_fine_unit)
+                                          run_slicing, dw_ms, args.pipeline_fine_unit, n_layers, H,
+                                          args.wgrad == "deferred")
         st.zero_grads()
+    out["mfma_probe_tflops"] = round(tp.measure_mfma_peak(), 1)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(params[0], x, dy, H, heads, args.cpu_baseline_tokens)
     print(json.dumps(out), flush=True)

@@ -216,6 +216,16 @@ typedef struct {
 tp_status tp_stage_enable_kernel_timing(tp_stage *stage, int enable);
 int tp_stage_kernel_stats(tp_stage *stage, tp_kernel_stat *out, int cap);
 
+/* Measurement helper: dense bf16 matrix-core throughput this device sustains.
+ * Runs, on the current device and the given stream (a hipStream_t, NULL =
+ * default), two workgroups of 4 waves per compute unit, each wave issuing
+ * `iters` x 8 independent 32x32x16 bf16 MFMAs with operands in registers (no
+ * memory traffic), after one untimed run, and writes the achieved TFLOP/s of
+ * the timed run to *tflops.  sink: device memory of >= 4 bytes per workgroup
+ * (2 x compute units), never written in practice (it keeps the work live).
+ * Synchronous.  Errors: TP_ERR_INVALID, TP_ERR_HIP. */
+tp_status tp_measure_mfma_peak(void *stream, int iters, void *sink, double *tflops);
+
 #ifdef __cplusplus
 }
 #endif

@@ -84,35 +84,44 @@ __device__ inline void dma16(const uint16_t* g, uint16_t* lds_wave_base) {
                                    0);
 }
 
-// Issue the DMA of one R x 64 operand tile into LDS (tile base `lds`).
-// KC: X(r, k) = X[r * ld + k]; MC: X(r, k) = X[k * ld + r].  Rows/columns past
-// rmax are clamped to valid memory (their products are never stored); k is
-// always in range (the caller guarantees whole k-tiles).
+// DMA of one R x BK operand tile into LDS.  KC: X(r, k) = X[r * ld + k];
+// MC: X(r, k) = X[k * ld + r].  Rows/columns past rmax are clamped to valid
+// memory (their products are never stored); k is always in range (the caller
+// guarantees whole k-tiles).  The per-lane part of every chunk address is a
+// byte offset from the k-origin of the tile, computed once per output tile;
+// each k-tile only moves the wave-uniform origin (X + k for KC, X + k * ld for
+// MC), so the loads take the scalar-base + 32-bit vector-offset form.  The
+// caller guarantees the offsets fit in 32 bits.
 template <int R, int BK, int NTH, bool KC>
-__device__ inline void dma_tile(const uint16_t* X, long ld, int r0, int rmax, int k0,
-                                uint16_t* lds) {
-  constexpr int CH = R * BK / 8 / NTH;  // 16-byte chunks per thread
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+struct DmaPlan {
+  static constexpr int CH = R * BK / 8 / NTH;  // 16-byte chunks per thread
+  uint32_t off[CH];
+  __device__ DmaPlan(long ld, int r0, int rmax, int w, int lane) {
 #pragma unroll
-  for (int i = 0; i < CH; ++i) {
-    const int s = i * NTH + w * 64 + lane;  // LDS slot of this lane
-    const uint16_t* g;
-    if constexpr (KC) {
-      constexpr int CPR = BK / 8;  // chunks per row
-      const int row = s / CPR, phys = s % CPR;
-      const int logical = phys ^ swz_kc<BK>(row);
-      const int gr = min(r0 + row, rmax - 1);
-      g = X + (long)gr * ld + k0 + logical * 8;
-    } else {
-      constexpr int CPR = R / 8;  // chunks per k-row
-      const int krow = s / CPR, phys = s % CPR;
-      const int logical = phys ^ swz_mc(krow);
-      const int gc = min(r0 + logical * 8, rmax - 8);
-      g = X + (long)(k0 + krow) * ld + gc;
+    for (int i = 0; i < CH; ++i) {
+      const int s = i * NTH + w * 64 + lane;  // LDS slot of this lane
+      if constexpr (KC) {
+        constexpr int CPR = BK / 8;  // chunks per row
+        const int row = s / CPR, phys = s % CPR;
+        const int logical = phys ^ swz_kc<BK>(row);
+        const int gr = min(r0 + row, rmax - 1);
+        off[i] = (uint32_t)(((long)gr * ld + logical * 8) * 2);
+      } else {
+        constexpr int CPR = R / 8;  // chunks per k-row
+        const int krow = s / CPR, phys = s % CPR;
+        const int logical = phys ^ swz_mc(krow);
+        const int gc = min(r0 + logical * 8, rmax - 8);
+        off[i] = (uint32_t)(((long)krow * ld + gc) * 2);
+      }
     }
-    dma16(g, lds + (i * NTH + w * 64) * 8);
   }
-}
+  // origin: X + k0 (KC) or X + k0 * ld (MC), wave-uniform; w: wave index (uniform)
+  __device__ void issue(const uint16_t* origin, uint16_t* lds, int w) const {
+#pragma unroll
+    for (int i = 0; i < CH; ++i)
+      dma16((const uint16_t*)((const char*)origin + off[i]), lds + (i * NTH + w * 64) * 8);
+  }
+};
 
 __device__ inline u32x4 ds_read128(uint32_t addr) {
   u32x4 v;
@@ -230,10 +239,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
     n0 = (tile % walk.tn) * BN;
   }
 
+  const int wu = __builtin_amdgcn_readfirstlane(wave);
+  const DmaPlan<BM, BK, NTH, A_KC> plan_a(lda, m0, a.M, wu, lane);
+  const DmaPlan<BN, BK, NTH, B_KC> plan_b(ldb, n0, a.N, wu, lane);
   auto issue = [&](int stage, int kt) {
     uint16_t* st = smem + stage * STAGE;
-    dma_tile<BM, BK, NTH, A_KC>(A, lda, m0, a.M, kbeg + kt * BK, st);
-    dma_tile<BN, BK, NTH, B_KC>(B, ldb, n0, a.N, kbeg + kt * BK, st + TILE_A);
+    const long k = kbeg + kt * BK;
+    plan_a.issue(A + (A_KC ? k : k * lda), st, wu);
+    plan_b.issue(B + (B_KC ? k : k * ldb), st + TILE_A, wu);
   };
 
   f32x16_t acc[FM][FN];
@@ -253,7 +266,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
     const int pending = min(STAGES - 2, nk - 1 - kt);
     wait_tiles<LPT, STAGES - 2>(pending);
     __builtin_amdgcn_s_barrier();
-    if (kt + STAGES - 1 < nk) issue((kt + STAGES - 1) % STAGES, kt + STAGES - 1);
 
     const uint32_t ta = sbase + (kt % STAGES) * STAGE * 2;
     const uint32_t tb = ta + TILE_A * 2;
@@ -286,6 +298,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
               __builtin_bit_cast(bf16x8_t, fa[cur][i]), __builtin_bit_cast(bf16x8_t, fb[cur][j]),
               acc[i][j], 0, 0, 0);
+      // the next k-tile's DMA goes out while the first step's MFMAs run; its
+      // stage was last read in the previous iteration, before the barrier
+      if (ks == 0 && kt + STAGES - 1 < nk) issue((kt + STAGES - 1) % STAGES, kt + STAGES - 1);
       if (ks + 1 < BK / 16) {
         // the next fragments must have arrived (their registers are tied to the wait)
         asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(fa[nxt][0]));
@@ -467,6 +482,9 @@ hipError_t gemm_dma_bf16_cfg(int cfg, const GemmArgs& a, hipStream_t s) {
   if (((uintptr_t)a.A & 15) || ((uintptr_t)a.B & 15)) return hipErrorNotSupported;
   const long lda = a_kc ? a.sam : a.sak, ldb = b_kc ? a.sbn : a.sbk;
   if ((lda & 7) || (ldb & 7)) return hipErrorNotSupported;
+  // per-lane DMA offsets are 32-bit byte offsets from a k-origin
+  auto fits = [](long rows, long ld) { return (rows + 1) * ld * 2 < (1l << 32); };
+  if (!fits(a_kc ? a.M : 64, lda) || !fits(b_kc ? a.N : 64, ldb)) return hipErrorNotSupported;
   // fp32 outputs leave as 16-byte row segments
   if (a.epi == EPI_ACC_F32 && (((uintptr_t)a.C & 15) || (a.ldc & 3))) return hipErrorNotSupported;
   if (cfg < 0) {

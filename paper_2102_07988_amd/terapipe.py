@@ -31,7 +31,7 @@ EXPORTED = ("tp_stage_workspace_bytes", "tp_stage_init", "tp_stage_destroy",
             "tp_kv_prefix_reset", "tp_slice_forward", "tp_slice_backward",
             "tp_profile_slice_cost", "tp_dp_optimal_slicing", "tp_fit_ctx_model",
             "tp_cost_table_from_model", "tp_profile_cost_model", "tp_status_string",
-            "tp_stage_enable_kernel_timing", "tp_stage_kernel_stats")
+            "tp_stage_enable_kernel_timing", "tp_stage_kernel_stats", "tp_measure_mfma_peak")
 
 
 class StageConfig(ctypes.Structure):
@@ -94,6 +94,8 @@ def _load():
     lib.tp_status_string.argtypes = [ctypes.c_int]
     lib.tp_stage_enable_kernel_timing.restype = ctypes.c_int
     lib.tp_stage_enable_kernel_timing.argtypes = [vp, ctypes.c_int]
+    lib.tp_measure_mfma_peak.restype = ctypes.c_int
+    lib.tp_measure_mfma_peak.argtypes = [vp, ctypes.c_int, vp, ctypes.POINTER(ctypes.c_double)]
     lib.tp_stage_kernel_stats.restype = ctypes.c_int
     lib.tp_stage_kernel_stats.argtypes = [vp, ctypes.POINTER(KernelStat), ctypes.c_int]
     return lib
@@ -313,6 +315,17 @@ def cost_table_from_model(t0: Sequence[int], unit: int, coef) -> np.ndarray:
     _check(lib.tp_cost_table_from_model(t0a.ctypes.data_as(i64p), U, unit, c,
                                         cost.ctypes.data_as(i64p)), "tp_cost_table_from_model")
     return cost
+
+
+def measure_mfma_peak(iters: int = 20000) -> float:
+    """Dense bf16 TFLOP/s of a register-only MFMA chain on every SIMD of cuda:0."""
+    import torch
+    sink = torch.empty(1 << 16, dtype=torch.float32, device="cuda")
+    out = ctypes.c_double()
+    _check(lib.tp_measure_mfma_peak(ctypes.c_void_p(torch.cuda.current_stream().cuda_stream), iters,
+                                    ctypes.c_void_p(sink.data_ptr()), ctypes.byref(out)),
+           "tp_measure_mfma_peak")
+    return out.value
 
 
 def slice_flops(n: int, c: int, hidden: int) -> int:

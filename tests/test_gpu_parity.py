@@ -172,3 +172,12 @@ def test_profile_cost_model_mode():
     # the DP runs on the model table
     lens, T = tp.dp_optimal_slicing(cost, unit, 8)
     assert sum(lens) == L and T > 0
+
+
+def test_mfma_peak_probe_plausible():
+    """The matrix-core probe reports a dense bf16 rate between a quarter of and
+    slightly above the nominal 2.5 PFLOP/s peak (a register-only MFMA chain)."""
+    from paper_2102_07988_amd import terapipe as tp
+    v = tp.measure_mfma_peak(2000)
+    print(f"mfma probe: {v:.1f} TFLOP/s", flush=True)
+    assert 600.0 < v < 2700.0
