@@ -206,8 +206,12 @@ struct TileWalk {
   }
 };
 
+// STAGES k-tiles of A and SB of B are buffered.  SB == STAGES: one ring of
+// (A, B) stages.  SB == STAGES + 1 == 3 ("B leads"): separate rings, the B
+// operand (the weights of a slice-shaped product, streamed from HBM) one
+// k-tile further ahead than A (activations, L2-resident).
 template <int BM, int BN, int BK, int WGM, int WGN, bool A_KC, bool B_KC, int EPI, bool SPLIT,
-          int STAGES>
+          int STAGES, int SB>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
   constexpr int NTH = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
@@ -216,6 +220,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
   static_assert(FM >= 1 && FN >= 1, "wave tile below 32 x 32");
   static_assert((BK * BM / 8) % NTH == 0 && (BK * BN / 8) % NTH == 0, "uneven DMA split");
   static_assert(LPT * (STAGES - 2) <= 63, "vmcnt range");
+  constexpr bool BLEAD = SB > STAGES;
+  static_assert(SB == STAGES || (STAGES == 2 && SB == 3), "unsupported ring shape");
+  constexpr int LPT_B = BK * BN / 8 / NTH;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
   const uint16_t* A = (const uint16_t*)a.A;
@@ -242,11 +249,27 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
   const int wu = __builtin_amdgcn_readfirstlane(wave);
   const DmaPlan<BM, BK, NTH, A_KC> plan_a(lda, m0, a.M, wu, lane);
   const DmaPlan<BN, BK, NTH, B_KC> plan_b(ldb, n0, a.N, wu, lane);
-  auto issue = [&](int stage, int kt) {
-    uint16_t* st = smem + stage * STAGE;
+  auto issue_a = [&](int kt) {
+    uint16_t* st = smem + (kt % STAGES) * (BLEAD ? TILE_A : STAGE);
     const long k = kbeg + kt * BK;
     plan_a.issue(A + (A_KC ? k : k * lda), st, wu);
-    plan_b.issue(B + (B_KC ? k : k * ldb), st + TILE_A, wu);
+  };
+  auto issue_b = [&](int kt) {
+    uint16_t* st = BLEAD ? smem + STAGES * TILE_A + (kt % SB) * TILE_B
+                         : smem + (kt % STAGES) * STAGE + TILE_A;
+    const long k = kbeg + kt * BK;
+    plan_b.issue(B + (B_KC ? k : k * ldb), st, wu);
+  };
+  // DMA of the k-tiles that iteration kt brings in (their stages were last read
+  // in iteration kt - 1, before its closing barrier)
+  auto issue_next = [&](int kt) {
+    if constexpr (BLEAD) {
+      if (kt + 1 < nk) issue_a(kt + 1);
+      if (kt + 2 < nk) issue_b(kt + 2);
+    } else if (kt + STAGES - 1 < nk) {
+      issue_a(kt + STAGES - 1);
+      issue_b(kt + STAGES - 1);
+    }
   };
 
   f32x16_t acc[FM][FN];
@@ -257,18 +280,39 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
+  if constexpr (BLEAD) {
+    // issue order B0, A0, B1, then per iteration A(kt+1), B(kt+2): when
+    // iteration kt starts, only B(kt+1) was issued after A(kt)
+    issue_b(0);
+    issue_a(0);
+    if (nk > 1) issue_b(1);
+  } else {
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
-    if (s < nk) issue(s, s);
+    for (int s = 0; s < STAGES - 1; ++s)
+      if (s < nk) {
+        issue_a(s);
+        issue_b(s);
+      }
+  }
 
   for (int kt = 0; kt < nk; ++kt) {
-    // k-tiles kt+1 .. kt+STAGES-2 may still be in flight; tile kt must have landed
-    const int pending = min(STAGES - 2, nk - 1 - kt);
-    wait_tiles<LPT, STAGES - 2>(pending);
+    if constexpr (BLEAD) {
+      if (kt + 1 < nk) wait_vm<LPT_B>();
+      else wait_vm<0>();
+    } else {
+      // k-tiles kt+1 .. kt+STAGES-2 may still be in flight; tile kt must have landed
+      const int pending = min(STAGES - 2, nk - 1 - kt);
+      wait_tiles<LPT, STAGES - 2>(pending);
+    }
     __builtin_amdgcn_s_barrier();
+    // split (slice-shaped, weight-streaming) products issue the next k-tiles'
+    // DMA at once; the others after the first step's MFMAs, which then run
+    // while the addresses go out
+    if (SPLIT) issue_next(kt);
 
-    const uint32_t ta = sbase + (kt % STAGES) * STAGE * 2;
-    const uint32_t tb = ta + TILE_A * 2;
+    const uint32_t ta = sbase + (kt % STAGES) * (BLEAD ? TILE_A : STAGE) * 2;
+    const uint32_t tb = BLEAD ? sbase + (STAGES * TILE_A + (kt % SB) * TILE_B) * 2
+                              : ta + TILE_A * 2;
     u32x4 fa[2][FM], fb[2][FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i) fa[0][i] = frag_read<BM, BK, A_KC>(ta, wm0 + 32 * i, 0, lane);
@@ -298,9 +342,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
               __builtin_bit_cast(bf16x8_t, fa[cur][i]), __builtin_bit_cast(bf16x8_t, fb[cur][j]),
               acc[i][j], 0, 0, 0);
-      // the next k-tile's DMA goes out while the first step's MFMAs run; its
-      // stage was last read in the previous iteration, before the barrier
-      if (ks == 0 && kt + STAGES - 1 < nk) issue((kt + STAGES - 1) % STAGES, kt + STAGES - 1);
+      // (the stage it fills was last read in the previous iteration, before the barrier)
+      if (!SPLIT && ks == 0) issue_next(kt);
       if (ks + 1 < BK / 16) {
         // the next fragments must have arrived (their registers are tied to the wait)
         asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(fa[nxt][0]));
@@ -317,8 +360,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
     // fp32 outputs: each 32 x 32 sub-tile goes through a wave-private LDS patch
     // (in the stage no wave reads in the last iteration) and leaves as 16-byte
     // row segments, two lanes per row.
-    static_assert(WGM * WGN * 32 * 36 * 4 <= STAGE * 2, "epilogue patch exceeds a stage");
-    float* patch = (float*)(smem + (nk % STAGES) * STAGE) + wave * (32 * 36);
+    // the patch takes the ring stage no wave reads in the last iteration, or,
+    // with separate rings, the LDS base once every wave has left the loop
+    static_assert(WGM * WGN * 32 * 36 * 4 <= (BLEAD ? STAGES * TILE_A : STAGE) * 2,
+                  "epilogue patch exceeds its region");
+    if constexpr (BLEAD) __builtin_amdgcn_s_barrier();
+    float* patch = (float*)(smem + (BLEAD ? 0 : (nk % STAGES) * STAGE)) + wave * (32 * 36);
     float* out = SPLIT ? a.ws + (long)blockIdx.z * a.M * a.N : (float*)a.C;
     const long ldo = SPLIT ? a.N : a.ldc;
     const int pr = lane >> 1, pc = (lane & 1) * 16;
@@ -380,10 +427,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
   }
 }
 
-template <int BM, int BN, int BK, int WGM, int WGN, bool A_KC, bool B_KC, int STAGES, bool SPLIT>
+template <int BM, int BN, int BK, int WGM, int WGN, bool A_KC, bool B_KC, int STAGES, int SB,
+          bool SPLIT>
 hipError_t launch_dma(const GemmArgs& a, hipStream_t s) {
   constexpr int NTH = 64 * WGM * WGN;
-  constexpr size_t lds = (size_t)STAGES * (BM + BN) * BK * 2;
+  constexpr size_t lds = ((size_t)STAGES * BM + (size_t)SB * BN) * BK * 2;
   dim3 grid(cdiv(a.N, BN), cdiv(a.M, BM), SPLIT ? a.splits : 1);
   if (!SPLIT && a.walk) {
     // rounds of 8 super-tiles (one per XCD), 256 workgroups per round
@@ -393,7 +441,7 @@ hipError_t launch_dma(const GemmArgs& a, hipStream_t s) {
   }
 #define TP_LAUNCH(E)                                                                         \
   do {                                                                                       \
-    auto* fn = gemm_dma_kernel<BM, BN, BK, WGM, WGN, A_KC, B_KC, E, SPLIT, STAGES>;        \
+    auto* fn = gemm_dma_kernel<BM, BN, BK, WGM, WGN, A_KC, B_KC, E, SPLIT, STAGES, SB>;    \
     static bool attr = false;                                                                \
     if (!attr) {                                                                             \
       hipError_t e = hipFuncSetAttribute((const void*)fn,                                    \
@@ -425,7 +473,8 @@ hipError_t launch_dma(const GemmArgs& a, hipStream_t s) {
 // LDS ring takes most of the 160 KB), so when the tile count is low the
 // reduction is split (<= 8 splits of >= 8 k-tiles; whole k-tiles, the last
 // split may be shorter) by the cost model below.
-template <int BM, int BN, int BK, int WGM, int WGN, bool A_KC, bool B_KC, int STAGES>
+template <int BM, int BN, int BK, int WGM, int WGN, bool A_KC, bool B_KC, int STAGES,
+          int SB = STAGES>
 hipError_t run_dma(GemmArgs a, hipStream_t s) {
   constexpr int CUS = 256;
   if (a.K % BK) return hipErrorNotSupported;
@@ -451,13 +500,13 @@ hipError_t run_dma(GemmArgs a, hipStream_t s) {
   if (splits > 1) {
     a.k_split = cdiv(nkt, splits) * BK;
     a.splits = cdiv(a.K, a.k_split);
-    hipError_t e = launch_dma<BM, BN, BK, WGM, WGN, A_KC, B_KC, STAGES, true>(a, s);
+    hipError_t e = launch_dma<BM, BN, BK, WGM, WGN, A_KC, B_KC, STAGES, SB, true>(a, s);
     if (e != hipSuccess) return e;
     return gemm_splitk_reduce(a, s);
   }
   // many tiles: XCD-aware super-tile order
   if (tiles >= 2 * CUS) a.walk = 1;
-  return launch_dma<BM, BN, BK, WGM, WGN, A_KC, B_KC, STAGES, false>(a, s);
+  return launch_dma<BM, BN, BK, WGM, WGN, A_KC, B_KC, STAGES, SB, false>(a, s);
 }
 
 template <bool A_KC, bool B_KC>
@@ -466,6 +515,7 @@ hipError_t run_cfg_id(int cfg, const GemmArgs& a, hipStream_t s) {
     case 0: return run_dma<128, 128, 64, 2, 2, A_KC, B_KC, 4>(a, s);
     case 1: return run_dma<256, 128, 64, 4, 2, A_KC, B_KC, 3>(a, s);
     case 2: return run_dma<256, 256, 64, 2, 4, A_KC, B_KC, 2>(a, s);
+    case 3: return run_dma<256, 256, 64, 2, 4, A_KC, B_KC, 2, 3>(a, s);
     default: return hipErrorNotSupported;
   }
 }
@@ -488,11 +538,14 @@ hipError_t gemm_dma_bf16_cfg(int cfg, const GemmArgs& a, hipStream_t s) {
   // fp32 outputs leave as 16-byte row segments
   if (a.epi == EPI_ACC_F32 && (((uintptr_t)a.C & 15) || (a.ldc & 3))) return hipErrorNotSupported;
   if (cfg < 0) {
-    // measured on the stage shapes: 256 x 256 tiles (2 stages) everywhere except
-    // small row counts and wide forward outputs, which prefer 256 x 128 (3 stages)
+    // measured on the stage shapes: 256 x 256 tiles everywhere except small row
+    // counts and wide forward outputs, which prefer 256 x 128 (3 stages); slice
+    // products (<= 256 rows, weights as B) keep the weight stream a k-tile
+    // further ahead than the activations
     if (a_mc && b_nc) cfg = 2;
     else if (a.M <= 128) cfg = 0;
     else if (a_kc && b_kc && a.M <= 256 && a.N >= 4 * a.K) cfg = 1;
+    else if (a.M <= 256) cfg = 3;
     else cfg = 2;
   }
   if (a_kc && b_kc) return run_cfg_id<true, true>(cfg, a, s);
