@@ -295,45 +295,63 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
       }
   }
 
-  for (int kt = 0; kt < nk; ++kt) {
+  // k-tile j has landed for every wave once at most the DMAs issued after it
+  // are in flight (they complete in issue order) and the workgroup has met at
+  // a barrier
+  auto wait_tile = [&](int j) {
     if constexpr (BLEAD) {
-      if (kt + 1 < nk) wait_vm<LPT_B>();
+      if (j + 1 < nk) wait_vm<LPT_B>();
       else wait_vm<0>();
     } else {
-      // k-tiles kt+1 .. kt+STAGES-2 may still be in flight; tile kt must have landed
-      const int pending = min(STAGES - 2, nk - 1 - kt);
-      wait_tiles<LPT, STAGES - 2>(pending);
+      wait_tiles<LPT, STAGES - 2>(min(STAGES - 2, nk - 1 - j));
     }
     __builtin_amdgcn_s_barrier();
-    // split (slice-shaped, weight-streaming) products issue the next k-tiles'
-    // DMA at once; the others after the first step's MFMAs, which then run
-    // while the addresses go out
-    if (SPLIT) issue_next(kt);
+  };
+  auto tile_a = [&](int j) { return sbase + (j % STAGES) * (BLEAD ? TILE_A : STAGE) * 2; };
+  auto tile_b = [&](int j) {
+    return BLEAD ? sbase + (STAGES * TILE_A + (j % SB) * TILE_B) * 2 : tile_a(j) + TILE_A * 2;
+  };
+  u32x4 fa[2][FM], fb[2][FN];
+  auto read_frags = [&](int buf, int j, int k0) {
+    const uint32_t ta = tile_a(j), tb = tile_b(j);
+#pragma unroll
+    for (int i = 0; i < FM; ++i) fa[buf][i] = frag_read<BM, BK, A_KC>(ta, wm0 + 32 * i, k0, lane);
+#pragma unroll
+    for (int jj = 0; jj < FN; ++jj) fb[buf][jj] = frag_read<BN, BK, B_KC>(tb, wn0 + 32 * jj, k0, lane);
+  };
+  // wait for every LDS read issued so far, every fragment register of `buf` tied to the wait
+  auto frags_ready = [&](int buf) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(fa[buf][0]));
+#pragma unroll
+    for (int i = 1; i < FM; ++i) asm volatile("" : "+v"(fa[buf][i]));
+#pragma unroll
+    for (int jj = 0; jj < FN; ++jj) asm volatile("" : "+v"(fb[buf][jj]));
+  };
 
-    const uint32_t ta = sbase + (kt % STAGES) * (BLEAD ? TILE_A : STAGE) * 2;
-    const uint32_t tb = BLEAD ? sbase + (STAGES * TILE_A + (kt % SB) * TILE_B) * 2
-                              : ta + TILE_A * 2;
-    u32x4 fa[2][FM], fb[2][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i) fa[0][i] = frag_read<BM, BK, A_KC>(ta, wm0 + 32 * i, 0, lane);
-#pragma unroll
-    for (int j = 0; j < FN; ++j) fb[0][j] = frag_read<BN, BK, B_KC>(tb, wn0 + 32 * j, 0, lane);
-    // first fragments: wait, with every fragment register tied to the wait
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(fa[0][0]));
-#pragma unroll
-    for (int i = 1; i < FM; ++i) asm volatile("" : "+v"(fa[0][i]));
-#pragma unroll
-    for (int j = 0; j < FN; ++j) asm volatile("" : "+v"(fb[0][j]));
+  // The k-tile boundary is software-pipelined: the barrier for tile kt+1 and
+  // its first fragment reads come before tile kt's last MFMA step, so those
+  // reads complete while that step runs.  The DMA of the tile after goes out
+  // right after the barrier for split (slice-shaped, weight-streaming)
+  // products, after the last MFMA step for the others; either way into the
+  // stage of tile kt, which every wave finished reading before the barrier.
+  wait_tile(0);
+  issue_next(0);
+  read_frags(0, 0, 0);
+  frags_ready(0);
+  for (int kt = 0; kt < nk; ++kt) {
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       const int cur = ks & 1, nxt = cur ^ 1;
-      if (ks + 1 < BK / 16) {
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-          fa[nxt][i] = frag_read<BM, BK, A_KC>(ta, wm0 + 32 * i, 16 * (ks + 1), lane);
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          fb[nxt][j] = frag_read<BN, BK, B_KC>(tb, wn0 + 32 * j, 16 * (ks + 1), lane);
+      const bool last = ks + 1 == BK / 16;
+      bool pending = true;
+      if (!last) {
+        read_frags(nxt, kt, 16 * (ks + 1));
+      } else if (kt + 1 < nk) {
+        wait_tile(kt + 1);
+        if (SPLIT) issue_next(kt + 1);
+        read_frags(nxt, kt + 1, 0);
+      } else {
+        pending = false;
       }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
@@ -342,75 +360,73 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
               __builtin_bit_cast(bf16x8_t, fa[cur][i]), __builtin_bit_cast(bf16x8_t, fb[cur][j]),
               acc[i][j], 0, 0, 0);
-      // (the stage it fills was last read in the previous iteration, before the barrier)
-      if (!SPLIT && ks == 0) issue_next(kt);
-      if (ks + 1 < BK / 16) {
-        // the next fragments must have arrived (their registers are tied to the wait)
-        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(fa[nxt][0]));
-#pragma unroll
-        for (int i = 1; i < FM; ++i) asm volatile("" : "+v"(fa[nxt][i]));
-#pragma unroll
-        for (int j = 0; j < FN; ++j) asm volatile("" : "+v"(fb[nxt][j]));
-      }
+      if (!SPLIT && last && kt + 1 < nk) issue_next(kt + 1);
+      if (pending) frags_ready(nxt);
     }
   }
   // every outstanding DMA has been waited for: the last iteration waited for 0
 
   if constexpr (SPLIT || EPI == EPI_ACC_F32) {
     // fp32 outputs: each 32 x 32 sub-tile goes through a wave-private LDS patch
-    // (in the stage no wave reads in the last iteration) and leaves as 16-byte
-    // row segments, two lanes per row.
-    // the patch takes the ring stage no wave reads in the last iteration, or,
-    // with separate rings, the LDS base once every wave has left the loop
+    // (in the ring stage no wave reads in the last iteration, or, with separate
+    // rings, at the LDS base once every wave has left the loop)
     static_assert(WGM * WGN * 32 * 36 * 4 <= (BLEAD ? STAGES * TILE_A : STAGE) * 2,
                   "epilogue patch exceeds its region");
     if constexpr (BLEAD) __builtin_amdgcn_s_barrier();
     float* patch = (float*)(smem + (BLEAD ? 0 : (nk % STAGES) * STAGE)) + wave * (32 * 36);
     float* out = SPLIT ? a.ws + (long)blockIdx.z * a.M * a.N : (float*)a.C;
     const long ldo = SPLIT ? a.N : a.ldc;
-    const int pr = lane >> 1, pc = (lane & 1) * 16;
+    // sub-tile rows leave as whole 128-byte lines: in step q (0..3) lane l
+    // takes row 8q + l/8, 16-byte chunk l%8
+    const int er = lane >> 3, ec = (lane & 7) * 4;
     const bool full = m0 + wm0 + WM <= a.M && n0 + wn0 + WN <= a.N;
-    auto dst_of = [&](int t) {
-      return out + (long)(m0 + wm0 + (t / FN) * 32 + pr) * ldo + n0 + wn0 + (t % FN) * 32 + pc;
+    auto dst_of = [&](int t, int q) {
+      return out + (long)(m0 + wm0 + (t / FN) * 32 + 8 * q + er) * ldo + n0 + wn0 + (t % FN) * 32 +
+             ec;
     };
-    float4 cur[4], nxt[4];
+    // fp32 +=: the destination values of the next P sub-tiles are in flight
+    // while one is combined
+    constexpr int T = FM * FN, P = T < 4 ? T : 4;
+    float4 pre[P][4];
     if (!SPLIT && full) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) cur[q] = *(const float4*)(dst_of(0) + 4 * q);
+      for (int t = 0; t < P; ++t)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) pre[t][q] = *(const float4*)dst_of(t, q);
     }
 #pragma unroll
-    for (int t = 0; t < FM * FN; ++t) {
+    for (int t = 0; t < T; ++t) {
       const int i = t / FN, j = t % FN;
-      // the next sub-tile's destination values are requested before this
-      // sub-tile is combined, so the read latency is paid about once
-      if (!SPLIT && full && t + 1 < FM * FN) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) nxt[q] = *(const float4*)(dst_of(t + 1) + 4 * q);
-      }
 #pragma unroll
       for (int v = 0; v < 16; ++v)
         patch[(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * 36 + (lane & 31)] = acc[i][j][v];
       float4 x[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) x[q] = *(const float4*)(patch + pr * 36 + pc + 4 * q);
-      const int m = m0 + wm0 + i * 32 + pr;
-      const int n = n0 + wn0 + j * 32 + pc;
-      float* dst = out + (long)m * ldo + n;
+      for (int q = 0; q < 4; ++q) x[q] = *(const float4*)(patch + (8 * q + er) * 36 + ec);
       if (full) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           if constexpr (!SPLIT) {
-            x[q].x += cur[q].x, x[q].y += cur[q].y, x[q].z += cur[q].z, x[q].w += cur[q].w;
+            const float4 o = pre[t % P][q];
+            x[q].x += o.x, x[q].y += o.y, x[q].z += o.z, x[q].w += o.w;
           }
-          *(float4*)(dst + 4 * q) = x[q];
+          *(float4*)dst_of(t, q) = x[q];
         }
-      } else if (m < a.M) {
-        const float* xs = (const float*)x;
-        for (int e = 0; e < 16 && n + e < a.N; ++e) dst[e] = SPLIT ? xs[e] : dst[e] + xs[e];
-      }
-      if (!SPLIT && full && t + 1 < FM * FN) {
+        if (!SPLIT && t + P < T) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) cur[q] = nxt[q];
+          for (int q = 0; q < 4; ++q) pre[t % P][q] = *(const float4*)dst_of(t + P, q);
+        }
+      } else {
+        const int n = n0 + wn0 + j * 32 + ec;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int m = m0 + wm0 + i * 32 + 8 * q + er;
+          if (m < a.M) {
+            float* dst = out + (long)m * ldo + n;
+            const float* xs = (const float*)&x[q];
+            for (int e = 0; e < 4 && n + e < a.N; ++e) dst[e] = SPLIT ? xs[e] : dst[e] + xs[e];
+          }
+        }
       }
     }
   } else {

@@ -181,3 +181,9 @@ def test_mfma_peak_probe_plausible():
     v = tp.measure_mfma_peak(2000)
     print(f"mfma probe: {v:.1f} TFLOP/s", flush=True)
     assert 600.0 < v < 2700.0
+
+
+def test_long_single_slice_many_heads():
+    """One 2048-token slice with 32 heads of width 64: long causal blocks in
+    forward, dK/dV and dQ, every attention grid at least two blocks per CU."""
+    _case(1, 2048, 32, 2048, "bf16", [2048], seeds=(31, 32, 33), label="long slice, 32 heads")
