@@ -264,23 +264,6 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
 // partials and of bf16 operands (bias, residual, z), 16-byte bf16 stores.
 // Requires N, every leading dimension and H to be multiples of 8 and every
 // pointer 16-byte aligned (checked by the launcher).
-__device__ inline void ld8(const bf16* p, float* x) {
-  const uint4 u = *(const uint4*)p;
-  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    x[2 * i] = __uint_as_float(w[i] << 16);
-    x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-  }
-}
-__device__ inline void st8(bf16* p, const float* x) {
-  uint32_t w[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-    w[i] = (uint32_t)f32_to_bf16_bits(x[2 * i]) | ((uint32_t)f32_to_bf16_bits(x[2 * i + 1]) << 16);
-  *(uint4*)p = make_uint4(w[0], w[1], w[2], w[3]);
-}
-
 template <int EPI>
 __global__ __launch_bounds__(256) void splitk_reduce8_kernel(GemmArgs a) {
   const long tot8 = (long)a.M * a.N / 8, plane = (long)a.M * a.N;
@@ -337,16 +320,6 @@ __global__ __launch_bounds__(256) void splitk_reduce8_kernel(GemmArgs a) {
   }
 }
 
-bool reduce8_ok(const GemmArgs& a) {
-  auto al = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
-  if (a.N % 8 || !al(a.ws) || !al(a.C) || a.ldc % 8) return false;
-  if (a.bias && !al(a.bias)) return false;
-  if ((a.epi == EPI_RESID || a.epi == EPI_DGELU) && (!al(a.R) || a.ldr % 8)) return false;
-  if (a.epi == EPI_GELU && (!al(a.C2) || a.ldc2 % 8)) return false;
-  if (a.epi == EPI_QKV && (a.H % 8 || !al(a.q) || !al(a.k) || !al(a.v))) return false;
-  return true;
-}
-
 template <int BM, int BN, int WGM, int WGN, bool A_KC, bool B_KC, bool SPLIT>
 hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
   dim3 grid(cdiv(a.N, BN), cdiv(a.M, BM), SPLIT ? a.splits : 1);
@@ -372,7 +345,7 @@ hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
 
 hipError_t launch_reduce(const GemmArgs& a, hipStream_t s) {
   const long tot = (long)a.M * a.N;
-  if (reduce8_ok(a)) {
+  if (vec8_ok(a)) {
     const int blocks = (int)std::min<long>(cdiv(tot / 8, 256), 4096);
     switch (a.epi) {
 #define TP_CASE(E) \
@@ -437,6 +410,18 @@ hipError_t launch_layout(const GemmArgs& a, hipStream_t s) {
 }
 
 }  // namespace
+
+// 8-column vector epilogues: N, every leading dimension and H multiples of 8,
+// every pointer 16-byte aligned
+bool vec8_ok(const GemmArgs& a) {
+  auto al = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
+  if (a.N % 8 || (a.ws && !al(a.ws)) || !al(a.C) || a.ldc % 8) return false;
+  if (a.bias && !al(a.bias)) return false;
+  if ((a.epi == EPI_RESID || a.epi == EPI_DGELU) && (!al(a.R) || a.ldr % 8)) return false;
+  if (a.epi == EPI_GELU && (!al(a.C2) || a.ldc2 % 8)) return false;
+  if (a.epi == EPI_QKV && (a.H % 8 || !al(a.q) || !al(a.k) || !al(a.v))) return false;
+  return true;
+}
 
 hipError_t gemm_splitk_reduce(const GemmArgs& a, hipStream_t s) { return launch_reduce(a, s); }
 

@@ -78,6 +78,46 @@ __device__ inline void epi_store(const GemmArgs& a, int m, int n, float acc) {
   }
 }
 
+// The bf16 epilogues for 8 consecutive columns n .. n+7 of row m (16-byte
+// accesses; the launcher checked sizes and alignment).
+template <int EPI>
+__device__ inline void epi_store8(const GemmArgs& a, int m, int n, float* x) {
+  if constexpr (EPI == EPI_DGELU) {
+    float z[8];
+    ld8((const bf16*)a.R + (long)m * a.ldr + n, z);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] *= gelu_tanh_grad(z[i]);
+    st8((bf16*)a.C + (long)m * a.ldc + n, x);
+  } else {
+    if (a.bias) {
+      float b[8];
+      ld8((const bf16*)a.bias + n, b);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) x[i] += b[i];
+    }
+    if constexpr (EPI == EPI_STORE) {
+      st8((bf16*)a.C + (long)m * a.ldc + n, x);
+    } else if constexpr (EPI == EPI_RESID) {
+      float r[8];
+      ld8((const bf16*)a.R + (long)m * a.ldr + n, r);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) x[i] += r[i];
+      st8((bf16*)a.C + (long)m * a.ldc + n, x);
+    } else if constexpr (EPI == EPI_GELU) {
+      st8((bf16*)a.C + (long)m * a.ldc + n, x);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) x[i] = gelu_tanh(x[i]);
+      st8((bf16*)a.C2 + (long)m * a.ldc2 + n, x);
+    } else if constexpr (EPI == EPI_QKV) {
+      const int H = a.H;
+      bf16* dst = n < H       ? (bf16*)a.q + (long)m * H + n
+                  : n < 2 * H ? (bf16*)a.k + (long)m * H + (n - H)
+                              : (bf16*)a.v + (long)m * H + (n - 2 * H);
+      st8(dst, x);
+    }
+  }
+}
+
 __device__ inline void dma16(const uint16_t* g, uint16_t* lds_wave_base) {
   __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
                                    (__attribute__((address_space(3))) void*)lds_wave_base, 16, 0,
@@ -423,23 +463,39 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
           const int m = m0 + wm0 + i * 32 + 8 * q + er;
           if (m < a.M) {
             float* dst = out + (long)m * ldo + n;
-            const float* xs = (const float*)&x[q];
-            for (int e = 0; e < 4 && n + e < a.N; ++e) dst[e] = SPLIT ? xs[e] : dst[e] + xs[e];
+            const float xs[4] = {x[q].x, x[q].y, x[q].z, x[q].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (n + e < a.N) dst[e] = SPLIT ? xs[e] : dst[e] + xs[e];
           }
         }
       }
     }
   } else {
+    // bf16 outputs: each 32 x 32 sub-tile goes through the LDS patch and leaves
+    // as 8-column row segments (in step q of 2, lane l takes row 16q + l/4,
+    // columns 8 (l%4) .. +7), one 16-byte access per operand; N % 8 == 0, so a
+    // segment is either inside the output or past its edge
+    if constexpr (BLEAD) __builtin_amdgcn_s_barrier();
+    float* patch = (float*)(smem + (BLEAD ? 0 : (nk % STAGES) * STAGE)) + wave * (32 * 36);
+    const int er = lane >> 2, ec = (lane & 3) * 8;
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
+      for (int j = 0; j < FN; ++j) {
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int m = m0 + wm0 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-          const int n = n0 + wn0 + j * 32 + (lane & 31);
-          if (m < a.M && n < a.N) epi_store<bf16, EPI>(a, m, n, acc[i][j][v]);
+        for (int v = 0; v < 16; ++v)
+          patch[(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * 36 + (lane & 31)] = acc[i][j][v];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const int r = 16 * q + er;
+          const float4 u = *(const float4*)(patch + r * 36 + ec);
+          const float4 w = *(const float4*)(patch + r * 36 + ec + 4);
+          float x[8] = {u.x, u.y, u.z, u.w, w.x, w.y, w.z, w.w};
+          const int m = m0 + wm0 + 32 * i + r, n = n0 + wn0 + 32 * j + ec;
+          if (m < a.M && n < a.N) epi_store8<EPI>(a, m, n, x);
         }
+      }
   }
 }
 
@@ -469,6 +525,13 @@ hipError_t launch_dma(const GemmArgs& a, hipStream_t s) {
   } while (0)
   if constexpr (SPLIT) {
     TP_LAUNCH(EPI_STORE);
+  } else if constexpr (!A_KC && !B_KC) {
+    // m/n-contiguous operands on both sides: the weight-gradient products
+    switch (a.epi) {
+      case EPI_STORE: TP_LAUNCH(EPI_STORE); break;
+      case EPI_ACC_F32: TP_LAUNCH(EPI_ACC_F32); break;
+      default: return hipErrorNotSupported;
+    }
   } else {
     switch (a.epi) {
       case EPI_STORE: TP_LAUNCH(EPI_STORE); break;
@@ -551,18 +614,19 @@ hipError_t gemm_dma_bf16_cfg(int cfg, const GemmArgs& a, hipStream_t s) {
   // per-lane DMA offsets are 32-bit byte offsets from a k-origin
   auto fits = [](long rows, long ld) { return (rows + 1) * ld * 2 < (1l << 32); };
   if (!fits(a_kc ? a.M : 64, lda) || !fits(b_kc ? a.N : 64, ldb)) return hipErrorNotSupported;
-  // fp32 outputs leave as 16-byte row segments
+  // fp32 outputs leave as 16-byte row segments, bf16 outputs (and their
+  // operands) as 8-column segments
   if (a.epi == EPI_ACC_F32 && (((uintptr_t)a.C & 15) || (a.ldc & 3))) return hipErrorNotSupported;
+  if (a.epi != EPI_ACC_F32 && !vec8_ok(a)) return hipErrorNotSupported;
   if (cfg < 0) {
     // measured on the stage shapes: 256 x 256 tiles everywhere except small row
-    // counts and wide forward outputs, which prefer 256 x 128 (3 stages); slice
-    // products (<= 256 rows, weights as B) keep the weight stream a k-tile
-    // further ahead than the activations
+    // counts and wide forward outputs of slices, which prefer 256 x 128 (3
+    // stages); products with the weights as B (activations or output gradients
+    // as A, k-contiguous) keep the weight stream a k-tile further ahead
     if (a_mc && b_nc) cfg = 2;
     else if (a.M <= 128) cfg = 0;
     else if (a_kc && b_kc && a.M <= 256 && a.N >= 4 * a.K) cfg = 1;
-    else if (a.M <= 256) cfg = 3;
-    else cfg = 2;
+    else cfg = 3;
   }
   if (a_kc && b_kc) return run_cfg_id<true, true>(cfg, a, s);
   if (a_kc && b_nc) return run_cfg_id<true, false>(cfg, a, s);

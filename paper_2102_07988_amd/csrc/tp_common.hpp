@@ -103,6 +103,24 @@ __device__ inline float block_max(float v, float* red) {
   return s;
 }
 
+// 8 consecutive bf16 values <-> fp32 (16-byte accesses; p 16-byte aligned)
+__device__ inline void ld8(const bf16* p, float* x) {
+  const uint4 u = *(const uint4*)p;
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[2 * i] = __uint_as_float(w[i] << 16);
+    x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+__device__ inline void st8(bf16* p, const float* x) {
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    w[i] = (uint32_t)f32_to_bf16_bits(x[2 * i]) | ((uint32_t)f32_to_bf16_bits(x[2 * i + 1]) << 16);
+  *(uint4*)p = make_uint4(w[0], w[1], w[2], w[3]);
+}
+
 __host__ __device__ inline int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
 
 }  // namespace tp

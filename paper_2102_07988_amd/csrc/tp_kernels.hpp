@@ -47,6 +47,8 @@ struct GemmArgs {
 };
 
 hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s);
+// host: the 8-column vector epilogues apply (sizes and alignment)
+bool vec8_ok(const GemmArgs& a);
 // Generic (any strides, any dtype) tiled FMA GEMM; the bf16 fast path falls back
 // to it for shapes it does not cover.
 hipError_t gemm_generic(int dtype, const GemmArgs& a, hipStream_t s);
