@@ -170,10 +170,17 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_mfma(AttnArgs a) {
 #pragma unroll
           for (int kk = 0; kk < KS; ++kk) s = mfma(kf[kk], qf[kk], s);
         }
+        // keys of a sub-block that ends at or before the wave's first query
+        // need no mask (all are <= every query of the wave and < r)
+        if (kbase + 32 * sb + 31 <= q_lo + 32 * w && kbase + 32 * sb + 32 <= a.r) {
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int key = kbase + 32 * sb + 8 * (v >> 2) + 4 * G + (v & 3);
-          p[sb][v] = (key <= t && key < a.r) ? s[v] * sl2 : -INFINITY;
+          for (int v = 0; v < 16; ++v) p[sb][v] = s[v] * sl2;
+        } else {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int key = kbase + 32 * sb + 8 * (v >> 2) + 4 * G + (v & 3);
+            p[sb][v] = (key <= t && key < a.r) ? s[v] * sl2 : -INFINITY;
+          }
         }
       }
       float mx = -INFINITY;
@@ -181,16 +188,23 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_mfma(AttnArgs a) {
       for (int v = 0; v < 16; ++v) mx = fmaxf(mx, fmaxf(p[0][v], p[1][v]));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       const float mnew = fmaxf(m, mx);
-      const float alpha = (mnew == -INFINITY) ? 1.f : exp2f(m - mnew);
-      float rs = 0.f;
+      float alpha = 1.f, rs = 0.f;
+      if (mnew == -INFINITY) {  // no visible key yet for this query (lane-uniform pair)
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
+        for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float e = (mnew == -INFINITY) ? 0.f : exp2f(p[sb][v] - mnew);
-          p[sb][v] = e;
-          rs += e;
-        }
+          for (int v = 0; v < 16; ++v) p[sb][v] = 0.f;
+      } else {
+        alpha = exp2f(m - mnew);
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const float e = exp2f(p[sb][v] - mnew);
+            p[sb][v] = e;
+            rs += e;
+          }
+      }
       rs += __shfl_xor(rs, 32, 64);
       lsum = lsum * alpha + rs;
       m = mnew;
