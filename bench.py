@@ -31,6 +31,9 @@ WORKLOADS = {
     "gpt3-13b-stage": (2, 5120, 40, 2048, [256] * 8),
     "gpt3-1.3b-stage": (2, 2048, 16, 2048, [256] * 8),
 }
+# pipeline depth K of the paper's setting for each model (Table 1: settings (2), (4), (10))
+PAPER_K = {"gpt3-175b-stage": 48, "gpt3-175b-stage-8k": 48, "gpt3-13b-stage": 20,
+           "gpt3-1.3b-stage": 12}
 
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
@@ -234,11 +237,15 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="gpt3-175b-stage", choices=sorted(WORKLOADS))
-    ap.add_argument("--slicing", default="", help="'uniform256' or comma-separated lengths")
+    ap.add_argument("--slicing", default="",
+                    help="'uniform256', comma-separated lengths, or 'dp' (DP over this stage's "
+                         "model-mode cost table at the paper's K for the model)")
     ap.add_argument("--wgrad", default="deferred", choices=["deferred", "per_slice"])
     ap.add_argument("--cpu-baseline-tokens", type=int, default=96)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--eager", action="store_true",
+                    help="time eager launches instead of a replayed HIP graph of the sequence")
     ap.add_argument("--no-pipeline", action="store_true",
                     help="skip the cost-table / DP / Eq. 5 pipeline-latency report")
     ap.add_argument("--pipeline-unit", type=int, default=128)
@@ -272,14 +279,34 @@ def main():
     from paper_2102_07988_amd import terapipe as tp
 
     n_layers, H, heads, L, default_sl = WORKLOADS[args.workload]
-    lens = parse_slicing(args.slicing, L, default_sl)
+    dp_source = None
+    lens = parse_slicing(args.slicing, L, default_sl) if args.slicing != "dp" else None
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    # the stage enqueues on its own stream (default priority), captured as a whole
+    cs = torch.cuda.Stream(device=dev)
+    torch.cuda.set_stream(cs)
     bf = torch.bfloat16
     params = synth.stage_params(n_layers, H, seed=synth.SEED_PARAMS, dtype=bf, device=dev)
     x = synth.hidden_states(L, H, seed=synth.SEED_X, dtype=bf, device=dev)
     dy = synth.upstream_grad(L, H, seed=synth.SEED_DY, dtype=bf, device=dev)
     st = tp.Stage(params, H, heads, L, dtype="bf16", wgrad=args.wgrad)
+    if lens is None:
+        # slicing chosen by the DP (Eq. 5-8, Algorithm 1) on this stage's own
+        # model-mode cost table (Eq. 9) at the paper's pipeline depth for the model
+        unit = max(16, L // 128)
+        U = L // unit
+        ks = sorted({k for k in (1, 2, U // 8, U // 4, U // 2, 3 * U // 4) if 1 <= k < U})
+        js = sorted({j for j in (1, U // 8, U // 4, U // 2, 3 * U // 4) if 1 <= j < U})
+        t0 = time.perf_counter()
+        cost, coef = st.profile_model(L, unit, [unit * k for k in ks], [unit * j for j in js],
+                                      warmup=1, reps=3)
+        prof_s = time.perf_counter() - t0
+        K = PAPER_K[args.workload]
+        lens, T = tp.dp_optimal_slicing(cost, unit, K)
+        st.zero_grads()
+        dp_source = {"kind": "dp", "table": "model mode (Eq. 9)", "unit": unit, "K": K,
+                     "predicted_T_ms": round(T / 1e6, 3), "profile_seconds": round(prof_s, 2)}
     y = torch.empty_like(x)
     dx = torch.empty_like(dy)
     bounds = [0]
@@ -295,20 +322,43 @@ def main():
             l, r = bounds[i], bounds[i + 1]
             st.backward(l, r, dy[l:r], out=dx[l:r])
 
-    for _ in range(args.warmup):
+    for _ in range(max(1, args.warmup)):
         step()
     torch.cuda.synchronize()
-    if not args.no_kernel_timing:
-        st.enable_kernel_timing(True)
-        st.kernel_stats()  # clears the counters
+    graph, graph_ok = None, None
+    if not args.eager:
+        # one whole sequence (reset, every slice forward and backward, the dW
+        # GEMMs) captured as a HIP graph and replayed per step: no launch gaps.
+        # Replays must reproduce the eager outputs bit for bit.
+        y_ref, dx_ref = y.clone(), dx.clone()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=cs):
+            step()
+        graph.replay()
+        torch.cuda.synchronize()
+        graph_ok = bool(torch.equal(y, y_ref) and torch.equal(dx, dx_ref))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        step()
+        if graph is not None:
+            graph.replay()
+        else:
+            step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    stats = st.kernel_stats() if not args.no_kernel_timing else {}
-    st.enable_kernel_timing(False)
+    if graph is not None:
+        graph_ok = graph_ok and bool(torch.equal(y, y_ref) and torch.equal(dx, dx_ref))
+    # per-kernel-class times: HIP events around every launch, in eager steps
+    # after the timed region (kernel durations do not depend on graph replay)
+    stats, kt_steps = {}, 0
+    if not args.no_kernel_timing:
+        kt_steps = min(args.steps, 3)
+        st.enable_kernel_timing(True)
+        st.kernel_stats()  # clears the counters
+        for _ in range(kt_steps):
+            step()
+        stats = st.kernel_stats()
+        st.enable_kernel_timing(False)
 
     flops_step = 0
     c = 0
@@ -324,7 +374,7 @@ def main():
     if stats:
         for name, s in stats.items():
             secs = max(s["total_ms"], 1e-9) * 1e-3
-            kernels[name] = {"launches": s["launches"], "ms_per_step": s["total_ms"] / args.steps,
+            kernels[name] = {"launches": s["launches"], "ms_per_step": s["total_ms"] / kt_steps,
                              "avg_us": 1e3 * s["total_ms"] / max(1, s["launches"]),
                              "achieved_tflops": round(s["flops"] / secs / 1e12, 2),
                              "achieved_gbs": round(s["bytes"] / secs / 1e9, 1)}
@@ -357,10 +407,13 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": args.workload, "layers": n_layers, "hidden": H, "heads": heads,
                    "seq_len": L, "batch": 1, "slicing": lens, "wgrad": args.wgrad,
+                   **({"slicing_source": dp_source} if dp_source else {}),
                    "global_batch": 1, "parallelism": "one pipeline stage"},
         "pct_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "flops_per_step": flops_step, "outputs_finite": finite,
         "roofline": roofline, "kernels": kernels,
+        "execution": "eager" if graph is None else "hip graph of one sequence, replayed per step",
+        "graph_matches_eager": graph_ok,
     }
     if not args.no_pipeline:
         dw_ms = kernels.get("gemm_bwd_dw_tn", {}).get("ms_per_step", 0.0) if args.wgrad == "deferred" else 0.0
