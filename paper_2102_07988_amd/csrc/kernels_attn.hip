@@ -111,8 +111,10 @@ struct Tile {
 
 // ------------------------------------------------------------------ forward
 
+// two waves per SIMD (registers capped at 256): one wave's softmax overlaps the
+// other's matrix products
 template <int D, int NW>
-__global__ __launch_bounds__(64 * NW) void attn_fwd_mfma(AttnArgs a) {
+__global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a) {
   using T = Tile<D>;
   constexpr int NTH = 64 * NW, BKV = 64, KS = D / 16, JB = D / 32, ST = 2;
   constexpr int TILE = BKV * D, STAGE = 2 * TILE;       // elements: K then V
@@ -441,7 +443,7 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_mfma(AttnArgs a) {
 // ------------------------------------------------------------------- dQ
 
 template <int D, int NW>
-__global__ __launch_bounds__(64 * NW) void attn_bwd_dq_mfma(AttnArgs a) {
+__global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a) {
   using T = Tile<D>;
   constexpr int NTH = 64 * NW, BKV = 64, KS = D / 16, JB = D / 32, ST = 2;
   constexpr int TILE = BKV * D, STAGE = 2 * TILE;  // K then V
@@ -492,23 +494,27 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_mfma(AttnArgs a) {
     for (int sb = 0; sb < 2; ++sb) {
       if (kbase + 32 * sb >= kend_w) break;
       f32x16_t s = zero16(), dp = zero16();
+      // K fragments, then V fragments in the same registers: the V reads go out
+      // once the S products have been issued
       {
-        u32x4 ka[KS], va[KS];
+        u32x4 ka[KS];
 #pragma unroll
-        for (int kk = 0; kk < KS; ++kk) {
-          ka[kk] = T::row8(Kt, 32 * sb + c, 2 * kk + G);
-          va[kk] = T::row8(Vt, 32 * sb + c, 2 * kk + G);
-        }
+        for (int kk = 0; kk < KS; ++kk) ka[kk] = T::row8(Kt, 32 * sb + c, 2 * kk + G);
         lgkm_wait(ka[0]);
 #pragma unroll
         for (int kk = 1; kk < KS; ++kk) lgkm_tie(ka[kk]);
 #pragma unroll
-        for (int kk = 0; kk < KS; ++kk) lgkm_tie(va[kk]);
+        for (int kk = 0; kk < KS; ++kk) s = mfma(ka[kk], qf[kk], s);
+      }
+      {
+        u32x4 va[KS];
 #pragma unroll
-        for (int kk = 0; kk < KS; ++kk) {
-          s = mfma(ka[kk], qf[kk], s);
-          dp = mfma(va[kk], of[kk], dp);
-        }
+        for (int kk = 0; kk < KS; ++kk) va[kk] = T::row8(Vt, 32 * sb + c, 2 * kk + G);
+        lgkm_wait(va[0]);
+#pragma unroll
+        for (int kk = 1; kk < KS; ++kk) lgkm_tie(va[kk]);
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) dp = mfma(va[kk], of[kk], dp);
       }
       f32x16_t ds;
 #pragma unroll
