@@ -266,9 +266,13 @@ __global__ __launch_bounds__(256) void attn_bwd_rowdot(AttnArgs a) {
 
 // ------------------------------------------------------------ dK / dV
 
-template <int D, int NW>
-__global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_mfma(AttnArgs a) {
+// MODE 0: dK and dV; 1: dV only (S, P, dV += P^T dO); 2: dK only (S, dP, dS,
+// dK += dS^T Q).  The single-output modes hold one accumulator set and fit
+// two waves per SIMD; together they recompute S once more than mode 0.
+template <int D, int NW, int MODE>
+__global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma(AttnArgs a) {
   using T = Tile<D>;
+  constexpr bool DO_K = MODE != 1, DO_V = MODE != 2;
   constexpr int NTH = 64 * NW, BQ = 32, KS = D / 16, JB = D / 32, ST = 2;
   constexpr int TILE = BQ * D;                           // elements
   constexpr int STAGE = 2 * TILE + NW * 128;             // Q, dO, then per-wave [lse | D]
@@ -284,13 +288,16 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_mfma(AttnArgs a) {
   const uint16_t* dO = (const uint16_t*)a.dout + h * D;
   const uint32_t sbase = lds_addr(smem);
 
+  // K fragments of the wave's keys stay in registers; V fragments (dK needs
+  // them for dP) are reloaded from L2 per query block in the dK-only mode
+  constexpr bool V_RESIDENT = MODE == 0;
   u32x4 kf[KS], vf[KS];
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) {
     kf[kk] = vf[kk] = u32x4{0, 0, 0, 0};
     if (s_me < a.r) {
       kf[kk] = *(const u32x4*)(Kc + (long)s_me * H + 16 * kk + 8 * G);
-      vf[kk] = *(const u32x4*)(Vc + (long)s_me * H + 16 * kk + 8 * G);
+      if constexpr (V_RESIDENT) vf[kk] = *(const u32x4*)(Vc + (long)s_me * H + 16 * kk + 8 * G);
     }
   }
   f32x16_t dk[JB], dv[JB];
@@ -327,30 +334,50 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_mfma(AttnArgs a) {
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
         lq[b] = ds_read128(LD + (8 * b + 4 * G) * 4);
-        dq4[b] = ds_read128(LD + 128 + (8 * b + 4 * G) * 4);
+        if constexpr (DO_K) dq4[b] = ds_read128(LD + 128 + (8 * b + 4 * G) * 4);
       }
       f32x16_t s = zero16(), dp = zero16();
       {
-        u32x4 qa[KS], oa[KS];
+        u32x4 qa[KS];
 #pragma unroll
-        for (int kk = 0; kk < KS; ++kk) {
-          qa[kk] = T::row8(Qt, c, 2 * kk + G);
-          oa[kk] = T::row8(Ot, c, 2 * kk + G);
-        }
+        for (int kk = 0; kk < KS; ++kk) qa[kk] = T::row8(Qt, c, 2 * kk + G);
         lgkm_wait(qa[0]);
 #pragma unroll
         for (int kk = 1; kk < KS; ++kk) lgkm_tie(qa[kk]);
 #pragma unroll
-        for (int kk = 0; kk < KS; ++kk) lgkm_tie(oa[kk]);
-#pragma unroll
         for (int b = 0; b < 4; ++b) {
           lgkm_tie(lq[b]);
-          lgkm_tie(dq4[b]);
+          if constexpr (DO_K) lgkm_tie(dq4[b]);
         }
 #pragma unroll
-        for (int kk = 0; kk < KS; ++kk) {
-          s = mfma(qa[kk], kf[kk], s);
-          dp = mfma(oa[kk], vf[kk], dp);
+        for (int kk = 0; kk < KS; ++kk) s = mfma(qa[kk], kf[kk], s);
+      }
+      if constexpr (DO_K && V_RESIDENT) {
+        u32x4 oa[KS];
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) oa[kk] = T::row8(Ot, c, 2 * kk + G);
+        lgkm_wait(oa[0]);
+#pragma unroll
+        for (int kk = 1; kk < KS; ++kk) lgkm_tie(oa[kk]);
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) dp = mfma(oa[kk], vf[kk], dp);
+      } else if constexpr (DO_K) {
+        // dP = dO V^T in two halves of the head width, V rows from L2
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          u32x4 oa[KS / 2], vr[KS / 2];
+#pragma unroll
+          for (int kk = 0; kk < KS / 2; ++kk) {
+            const int k2 = hf * (KS / 2) + kk;
+            vr[kk] = s_me < a.r ? *(const u32x4*)(Vc + (long)s_me * H + 16 * k2 + 8 * G)
+                                : u32x4{0, 0, 0, 0};
+            oa[kk] = T::row8(Ot, c, 2 * k2 + G);
+          }
+          lgkm_wait(oa[0]);
+#pragma unroll
+          for (int kk = 1; kk < KS / 2; ++kk) lgkm_tie(oa[kk]);
+#pragma unroll
+          for (int kk = 0; kk < KS / 2; ++kk) dp = mfma(oa[kk], vr[kk], dp);
         }
       }
       // s[v], dp[v]: query row qi = 8 (v / 4) + 4 G + v % 4 of the block, key s_me
@@ -361,29 +388,33 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_mfma(AttnArgs a) {
         const int tq = a.l + i0 + qi;
         const bool ok = qi < qval && s_me <= tq;
         const float lse_q = __uint_as_float(lq[v >> 2][v & 3]);
-        const float D_q = __uint_as_float(dq4[v >> 2][v & 3]);
         const float pv = ok ? exp2f(s[v] * sl2 - lse_q * LOG2E) : 0.f;
         p[v] = pv;
-        ds[v] = pv * (dp[v] - D_q);
+        if constexpr (DO_K) ds[v] = pv * (dp[v] - __uint_as_float(dq4[v >> 2][v & 3]));
       }
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-        const u32x4 pb = acc_half_bf16(p, ks), db = acc_half_bf16(ds, ks);
-        u32x4 ob[JB], qb2[JB];
+        if constexpr (DO_V) {
+          const u32x4 pb = acc_half_bf16(p, ks);
+          u32x4 ob[JB];
 #pragma unroll
-        for (int j = 0; j < JB; ++j) {
-          ob[j] = T::col8(Ot, 16 * ks, 32 * j, lane);
-          qb2[j] = T::col8(Qt, 16 * ks, 32 * j, lane);
+          for (int j = 0; j < JB; ++j) ob[j] = T::col8(Ot, 16 * ks, 32 * j, lane);
+          lgkm_wait(ob[0]);
+#pragma unroll
+          for (int j = 1; j < JB; ++j) lgkm_tie(ob[j]);
+#pragma unroll
+          for (int j = 0; j < JB; ++j) dv[j] = mfma(pb, ob[j], dv[j]);
         }
-        lgkm_wait(ob[0]);
+        if constexpr (DO_K) {
+          const u32x4 db = acc_half_bf16(ds, ks);
+          u32x4 qb2[JB];
 #pragma unroll
-        for (int j = 1; j < JB; ++j) lgkm_tie(ob[j]);
+          for (int j = 0; j < JB; ++j) qb2[j] = T::col8(Qt, 16 * ks, 32 * j, lane);
+          lgkm_wait(qb2[0]);
 #pragma unroll
-        for (int j = 0; j < JB; ++j) lgkm_tie(qb2[j]);
+          for (int j = 1; j < JB; ++j) lgkm_tie(qb2[j]);
 #pragma unroll
-        for (int j = 0; j < JB; ++j) {
-          dv[j] = mfma(pb, ob[j], dv[j]);
-          dk[j] = mfma(db, qb2[j], dk[j]);
+          for (int j = 0; j < JB; ++j) dk[j] = mfma(db, qb2[j], dk[j]);
         }
       }
     }
@@ -399,8 +430,8 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_mfma(AttnArgs a) {
     float ck[16], cv[16];
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      ck[v] = dkb[rowoff(v)];
-      cv[v] = dvb[rowoff(v)];
+      if constexpr (DO_K) ck[v] = dkb[rowoff(v)];
+      if constexpr (DO_V) cv[v] = dvb[rowoff(v)];
     }
 #pragma unroll
     for (int j = 0; j < JB; ++j) {
@@ -408,20 +439,20 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_mfma(AttnArgs a) {
       if (j + 1 < JB) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          nk[v] = dkb[rowoff(v) + 32 * (j + 1)];
-          nv[v] = dvb[rowoff(v) + 32 * (j + 1)];
+          if constexpr (DO_K) nk[v] = dkb[rowoff(v) + 32 * (j + 1)];
+          if constexpr (DO_V) nv[v] = dvb[rowoff(v) + 32 * (j + 1)];
         }
       }
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        dkb[rowoff(v) + 32 * j] = ck[v] + dk[j][v] * a.scale;
-        dvb[rowoff(v) + 32 * j] = cv[v] + dv[j][v];
+        if constexpr (DO_K) dkb[rowoff(v) + 32 * j] = ck[v] + dk[j][v] * a.scale;
+        if constexpr (DO_V) dvb[rowoff(v) + 32 * j] = cv[v] + dv[j][v];
       }
       if (j + 1 < JB) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          ck[v] = nk[v];
-          cv[v] = nv[v];
+          if constexpr (DO_K) ck[v] = nk[v];
+          if constexpr (DO_V) cv[v] = nv[v];
         }
       }
     }
@@ -433,8 +464,8 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_mfma(AttnArgs a) {
         const int key = s_w + 8 * (v >> 2) + 4 * G + (v & 3);
         if (key < a.r) {
           const long off = (long)key * H + h * D + 32 * j + c;
-          a.dk[off] += dk[j][v] * a.scale;
-          a.dv[off] += dv[j][v];
+          if constexpr (DO_K) a.dk[off] += dk[j][v] * a.scale;
+          if constexpr (DO_V) a.dv[off] += dv[j][v];
         }
       }
   }
@@ -553,6 +584,11 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a) {
 }
 
 constexpr int NWF = 4;  // waves per block
+// dK/dV as one kernel (0) or as a dV kernel (1) followed by a dK kernel (2)
+#ifndef TP_DKDV_MODE_A
+#define TP_DKDV_MODE_A 1
+#endif
+constexpr int DKDV_MODE_A = TP_DKDV_MODE_A;
 
 template <typename K>
 hipError_t set_lds(K* fn, size_t bytes) {
@@ -578,11 +614,15 @@ hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   constexpr size_t lds_kv = 2 * (2 * 32 * D + NWF * 128) * 2;
-  e = set_lds(attn_bwd_dkdv_mfma<D, NWF>, lds_kv);
-  if (e != hipSuccess) return e;
-  attn_bwd_dkdv_mfma<D, NWF><<<dim3(cdiv(a.r, 32 * NWF), a.heads), 64 * NWF, lds_kv, s>>>(a);
+  const dim3 grid_kv(cdiv(a.r, 32 * NWF), a.heads);
+  attn_bwd_dkdv_mfma<D, NWF, DKDV_MODE_A><<<grid_kv, 64 * NWF, lds_kv, s>>>(a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if constexpr (DKDV_MODE_A != 0) {
+    attn_bwd_dkdv_mfma<D, NWF, 2><<<grid_kv, 64 * NWF, lds_kv, s>>>(a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   constexpr size_t lds_q = 2 * 2 * 64 * D * 2;
   e = set_lds(attn_bwd_dq_mfma<D, NWF>, lds_q);
   if (e != hipSuccess) return e;
