@@ -50,9 +50,17 @@ __device__ inline f32x16_t zero16() {
   return z;
 }
 
+// Two fp32 values as round-to-nearest-even bf16 (lo in the low half), one
+// v_cvt_pk_bf16_f32.
 __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
-  return (uint32_t)f32_to_bf16_bits(lo) | ((uint32_t)f32_to_bf16_bits(hi) << 16);
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
 }
+
+// 2^x as the bare v_exp_f32 (results below the normal range flush to 0, which
+// a softmax weight may do).
+__device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // 8 accumulator values (one reduction half) as a bf16 operand.
 __device__ inline u32x4 acc_half_bf16(const f32x16_t& x, int ks) {
@@ -137,6 +145,13 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a) {
     qf[kk] = u32x4{0, 0, 0, 0};
     if (tvalid) qf[kk] = *(const u32x4*)(Q + (long)(t - a.l) * H + h * D + 16 * kk + 8 * G);
   }
+  // Online softmax in the log2 domain.  m is the reference maximum of the
+  // lane's scaled scores (log2 units); it moves only when a block's maximum
+  // exceeds it by more than RESCALE_LOG2 (and then for the whole wave), so the
+  // O and lsum rescale is skipped for most blocks.  The unnormalised weights
+  // stay below 2^RESCALE_LOG2, and O / lsum and lse are unchanged in exact
+  // arithmetic.
+  constexpr float RESCALE_LOG2 = 8.f;
   const float sl2 = a.scale * LOG2E;
   float m = -INFINITY, lsum = 0.f;
   f32x16_t o[JB];
@@ -158,7 +173,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a) {
     const int kbase = kb * BKV;
     if (kbase < kend_w) {
       const uint32_t Kt = sbase + (kb % ST) * STAGE * 2, Vt = Kt + TILE * 2;
-      f32x16_t p[2];
+      f32x16_t p[2];  // raw scores, -inf where masked
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb) {
         f32x16_t s = zero16();
@@ -175,45 +190,44 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a) {
         // keys of a sub-block that ends at or before the wave's first query
         // need no mask (all are <= every query of the wave and < r)
         if (kbase + 32 * sb + 31 <= q_lo + 32 * w && kbase + 32 * sb + 32 <= a.r) {
-#pragma unroll
-          for (int v = 0; v < 16; ++v) p[sb][v] = s[v] * sl2;
+          p[sb] = s;
         } else {
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const int key = kbase + 32 * sb + 8 * (v >> 2) + 4 * G + (v & 3);
-            p[sb][v] = (key <= t && key < a.r) ? s[v] * sl2 : -INFINITY;
+            p[sb][v] = (key <= t && key < a.r) ? s[v] : -INFINITY;
           }
         }
       }
       float mx = -INFINITY;
 #pragma unroll
       for (int v = 0; v < 16; ++v) mx = fmaxf(mx, fmaxf(p[0][v], p[1][v]));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mnew = fmaxf(m, mx);
-      float alpha = 1.f, rs = 0.f;
-      if (mnew == -INFINITY) {  // no visible key yet for this query (lane-uniform pair)
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * sl2;
+      if (__builtin_amdgcn_ballot_w64(mx > m + RESCALE_LOG2) != 0) {  // wave-uniform
+        const float mnew = fmaxf(m, mx);
+        // no visible key yet for this query (both stay -inf): nothing to scale
+        const float alpha = mnew == -INFINITY ? 1.f : exp2_fast(m - mnew);
+        lsum *= alpha;
 #pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
+        for (int j = 0; j < JB; ++j)
 #pragma unroll
-          for (int v = 0; v < 16; ++v) p[sb][v] = 0.f;
-      } else {
-        alpha = exp2f(m - mnew);
-#pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const float e = exp2f(p[sb][v] - mnew);
-            p[sb][v] = e;
-            rs += e;
-          }
+          for (int v = 0; v < 16; ++v) o[j][v] *= alpha;
+        m = mnew;
       }
+      // weights 2^(s sl2 - m); a lane with no visible key so far has only
+      // masked scores (-inf) and gets zeros
+      const float moff = m == -INFINITY ? 0.f : -m;
+      float rs = 0.f;
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float e = exp2_fast(__builtin_fmaf(p[sb][v], sl2, moff));
+          p[sb][v] = e;
+          rs += e;
+        }
       rs += __shfl_xor(rs, 32, 64);
-      lsum = lsum * alpha + rs;
-      m = mnew;
-#pragma unroll
-      for (int j = 0; j < JB; ++j)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) o[j][v] *= alpha;
+      lsum += rs;
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb) {
         if (kbase + 32 * sb >= kend_w) break;
@@ -388,7 +402,7 @@ __global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma
         const int tq = a.l + i0 + qi;
         const bool ok = qi < qval && s_me <= tq;
         const float lse_q = __uint_as_float(lq[v >> 2][v & 3]);
-        const float pv = ok ? exp2f(s[v] * sl2 - lse_q * LOG2E) : 0.f;
+        const float pv = ok ? exp2_fast(__builtin_fmaf(s[v], sl2, -lse_q * LOG2E)) : 0.f;
         p[v] = pv;
         if constexpr (DO_K) ds[v] = pv * (dp[v] - __uint_as_float(dq4[v >> 2][v & 3]));
       }
@@ -552,7 +566,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a) {
       for (int v = 0; v < 16; ++v) {
         const int key = kbase + 32 * sb + 8 * (v >> 2) + 4 * G + (v & 3);
         const bool ok = tvalid && key <= t;
-        const float pv = ok ? exp2f(s[v] * sl2 - lse2) : 0.f;
+        const float pv = ok ? exp2_fast(__builtin_fmaf(s[v], sl2, -lse2)) : 0.f;
         ds[v] = pv * (dp[v] - Dt);
       }
 #pragma unroll

@@ -259,45 +259,57 @@ __device__ inline void store8(float* p, const float* v) {
   ((float4*)p)[1] = make_float4(v[4], v[5], v[6], v[7]);
 }
 
-// One block of 256 threads per row; the row stays in registers (H <= 16384,
-// H % 8 == 0): thread t owns the 8-element chunks t, t + 256, ...
-constexpr int LN_MAXC = 8;
+// One block per row; the row stays in registers (H % 8 == 0, H <= 16384).  The
+// block has nt threads (a multiple of 64, <= 1024) and thread t owns the
+// 8-element chunks t + nt * c, c < CPT; CPT = 2 only when H / 8 > 1024.  Every
+// load a thread makes (row, gamma, beta, residual) is issued before the first
+// reduction, so a row costs one memory latency instead of several.
+struct LnShape {
+  int cpt, nt;
+};
+inline LnShape ln_shape(int H) {
+  const int nc = H / 8, cpt = nc > 1024 ? 2 : 1;
+  return {cpt, cdiv(cdiv(nc, cpt), 64) * 64};
+}
 
-template <typename T>
-__global__ __launch_bounds__(256) void ln_fwd_kernel(int H, const T* x, T* x_copy, const T* g,
-                                                     const T* b, T* u, float* mean, float* rstd,
-                                                     float eps) {
+template <typename T, int CPT>
+__global__ __launch_bounds__(1024) void ln_fwd_kernel(int H, const T* x, T* x_copy, const T* g,
+                                                      const T* b, T* u, float* mean, float* rstd,
+                                                      float eps) {
   __shared__ float red[16];
-  const int row = blockIdx.x, nc = H >> 3;
+  const int row = blockIdx.x, nc = H >> 3, nt = blockDim.x;
   const T* xr = x + (long)row * H;
-  float v[LN_MAXC][8];
-  float s = 0.f;
+  float v[CPT][8], gg[CPT][8], bb[CPT][8];
 #pragma unroll
-  for (int c = 0; c < LN_MAXC; ++c) {
-    const int ci = threadIdx.x + 256 * c;
+  for (int c = 0; c < CPT; ++c) {
+    const int ci = threadIdx.x + nt * c;
     if (ci < nc) {
       load8(xr + ci * 8, v[c]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) s += v[c][e];
+      load8(g + ci * 8, gg[c]);
+      load8(b + ci * 8, bb[c]);
     }
   }
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < CPT; ++c)
+    if (threadIdx.x + nt * c < nc)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s += v[c][e];
   const float mu = block_sum(s, red) / H;
   float q = 0.f;
 #pragma unroll
-  for (int c = 0; c < LN_MAXC; ++c)
-    if (threadIdx.x + 256 * c < nc)
+  for (int c = 0; c < CPT; ++c)
+    if (threadIdx.x + nt * c < nc)
 #pragma unroll
       for (int e = 0; e < 8; ++e) q += (v[c][e] - mu) * (v[c][e] - mu);
   const float rs = rsqrtf(block_sum(q, red) / H + eps);
 #pragma unroll
-  for (int c = 0; c < LN_MAXC; ++c) {
-    const int ci = threadIdx.x + 256 * c;
+  for (int c = 0; c < CPT; ++c) {
+    const int ci = threadIdx.x + nt * c;
     if (ci < nc) {
-      float gg[8], bb[8], o[8];
-      load8(g + ci * 8, gg);
-      load8(b + ci * 8, bb);
+      float o[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o[e] = gg[e] * ((v[c][e] - mu) * rs) + bb[e];
+      for (int e = 0; e < 8; ++e) o[e] = gg[c][e] * ((v[c][e] - mu) * rs) + bb[c][e];
       store8(u + (long)row * H + ci * 8, o);
       if (x_copy) store8(x_copy + (long)row * H + ci * 8, v[c]);
     }
@@ -308,70 +320,115 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(int H, const T* x, T* x_cop
   }
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void ln_bwd_kernel(int H, const T* du, const T* x,
-                                                     const float* mean, const float* rstd,
-                                                     const T* g, const T* resid, T* dx) {
-  __shared__ float red[16];
-  const int row = blockIdx.x, nc = H >> 3;
+// Two block-wide sums in one pass (blockDim.x a multiple of 64, <= 1024).
+__device__ inline float2 block_sum2(float a, float b, float* red /* >= 32 floats */) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  a = wave_sum(a);
+  b = wave_sum(b);
+  if (lane == 0) red[w] = a, red[16 + w] = b;
+  __syncthreads();
+  float sa = 0.f, sb = 0.f;
+  for (int i = 0; i < nw; ++i) sa += red[i], sb += red[16 + i];
+  return make_float2(sa, sb);
+}
+
+template <typename T, int CPT>
+__global__ __launch_bounds__(1024) void ln_bwd_kernel(int H, const T* du, const T* x,
+                                                      const float* mean, const float* rstd,
+                                                      const T* g, const T* resid, T* dx) {
+  __shared__ float red[32];
+  const int row = blockIdx.x, nc = H >> 3, nt = blockDim.x;
   const float mu = mean[row], rs = rstd[row];
-  float xh[LN_MAXC][8], dg[LN_MAXC][8];
+  float xh[CPT][8], dg[CPT][8], r[CPT][8];
+#pragma unroll
+  for (int c = 0; c < CPT; ++c) {
+    const int ci = threadIdx.x + nt * c;
+    if (ci < nc) {
+      float gg[8];
+      load8(x + (long)row * H + ci * 8, xh[c]);
+      load8(du + (long)row * H + ci * 8, dg[c]);
+      load8(g + ci * 8, gg);
+      if (resid) load8(resid + (long)row * H + ci * 8, r[c]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dg[c][e] *= gg[e];
+    }
+  }
   float sa = 0.f, sb = 0.f;
 #pragma unroll
-  for (int c = 0; c < LN_MAXC; ++c) {
-    const int ci = threadIdx.x + 256 * c;
-    if (ci < nc) {
-      float d[8], gg[8];
-      load8(x + (long)row * H + ci * 8, xh[c]);
-      load8(du + (long)row * H + ci * 8, d);
-      load8(g + ci * 8, gg);
+  for (int c = 0; c < CPT; ++c)
+    if (threadIdx.x + nt * c < nc)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         xh[c][e] = (xh[c][e] - mu) * rs;
-        dg[c][e] = d[e] * gg[e];
         sa += dg[c][e];
         sb += dg[c][e] * xh[c][e];
       }
-    }
-  }
-  const float a = block_sum(sa, red) / H;
-  const float bm = block_sum(sb, red) / H;
+  const float2 ab = block_sum2(sa, sb, red);
+  const float a = ab.x / H, bm = ab.y / H;
 #pragma unroll
-  for (int c = 0; c < LN_MAXC; ++c) {
-    const int ci = threadIdx.x + 256 * c;
+  for (int c = 0; c < CPT; ++c) {
+    const int ci = threadIdx.x + nt * c;
     if (ci < nc) {
-      float o[8], r[8];
-      if (resid) load8(resid + (long)row * H + ci * 8, r);
+      float o[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o[e] = rs * (dg[c][e] - a - xh[c][e] * bm) + (resid ? r[e] : 0.f);
+      for (int e = 0; e < 8; ++e)
+        o[e] = rs * (dg[c][e] - a - xh[c][e] * bm) + (resid ? r[c][e] : 0.f);
       store8(dx + (long)row * H + ci * 8, o);
     }
   }
 }
 
-// Column reductions: a block owns 64 columns (8 chunks of 8) and 32 row groups;
-// row group rg sums rows rg, rg + 32, ... in order, then the 32 partial sums
-// are added in row-group order.  Deterministic.
+// Column reductions over n rows.  A block owns 32 columns (4 chunks of 8) and
+// 64 row groups; row group rg sums rows rg, rg + 64, ... in order, loading four
+// rows at a time, then the 64 partial sums of a column are added as 8 in-order
+// groups of 8, the group sums in order.  Deterministic.
+constexpr int CR_RG = 64, CR_COLS = 32, CR_UNROLL = 4;
+
+// Adds the 64 per-row-group partials of each of the block's 32 columns (in
+// p[rg][col]) and returns the column total in threads 0..31.
+__device__ inline float col_partials_sum(float (*p)[CR_COLS + 1], float* q /* 8 x 33 */) {
+  const int col = threadIdx.x & 31, grp = threadIdx.x >> 5;
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) s += p[grp * 8 + i][col];
+  q[grp * (CR_COLS + 1) + col] = s;
+  __syncthreads();
+  float t = 0.f;
+  if (threadIdx.x < CR_COLS)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) t += q[i * (CR_COLS + 1) + col];
+  return t;
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void ln_param_grads_kernel(int n, int H, const T* du,
                                                              const T* x, const float* mean,
                                                              const float* rstd, float* dg,
                                                              float* db) {
-  __shared__ float pg[32][65], pb[32][65];
-  const int cc = threadIdx.x & 7, rg = threadIdx.x >> 3;
-  const int c0 = blockIdx.x * 64 + cc * 8;
+  __shared__ float pg[CR_RG][CR_COLS + 1], pb[CR_RG][CR_COLS + 1], q[2][8 * (CR_COLS + 1)];
+  const int cc = threadIdx.x & 3, rg = threadIdx.x >> 2;
+  const int c0 = blockIdx.x * CR_COLS + cc * 8;
   float sg[8] = {}, sb[8] = {};
   if (c0 < H) {
-    for (int t = rg; t < n; t += 32) {
-      float d[8], xv[8];
-      load8(du + (long)t * H + c0, d);
-      load8(x + (long)t * H + c0, xv);
-      const float mu = mean[t], rs = rstd[t];
+    for (int t0 = rg; t0 < n; t0 += CR_UNROLL * CR_RG) {
+      float d[CR_UNROLL][8], xv[CR_UNROLL][8], mu[CR_UNROLL], rs[CR_UNROLL];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        sg[e] += d[e] * ((xv[e] - mu) * rs);
-        sb[e] += d[e];
+      for (int k = 0; k < CR_UNROLL; ++k) {
+        const int t = t0 + k * CR_RG;
+        if (t < n) {
+          load8(du + (long)t * H + c0, d[k]);
+          load8(x + (long)t * H + c0, xv[k]);
+          mu[k] = mean[t], rs[k] = rstd[t];
+        }
       }
+#pragma unroll
+      for (int k = 0; k < CR_UNROLL; ++k)
+        if (t0 + k * CR_RG < n)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            sg[e] += d[k][e] * ((xv[k][e] - mu[k]) * rs[k]);
+            sb[e] += d[k][e];
+          }
     }
   }
 #pragma unroll
@@ -380,55 +437,56 @@ __global__ __launch_bounds__(256) void ln_param_grads_kernel(int n, int H, const
     pb[rg][cc * 8 + e] = sb[e];
   }
   __syncthreads();
-  if (threadIdx.x < 64) {
-    const int col = blockIdx.x * 64 + threadIdx.x;
-    if (col < H) {
-      float a = 0.f, b = 0.f;
-      for (int r = 0; r < 32; ++r) {
-        a += pg[r][threadIdx.x];
-        b += pb[r][threadIdx.x];
-      }
-      dg[col] += a;
-      db[col] += b;
-    }
+  const float a = col_partials_sum(pg, q[0]);
+  const float b = col_partials_sum(pb, q[1]);
+  const int col = blockIdx.x * CR_COLS + threadIdx.x;
+  if (threadIdx.x < CR_COLS && col < H) {
+    dg[col] += a;
+    db[col] += b;
   }
 }
 
 template <typename T>
 __global__ __launch_bounds__(256) void colsum_kernel(int n, int N, const T* A, long lda,
                                                      float* out) {
-  __shared__ float ps[32][65];
-  const int cc = threadIdx.x & 7, rg = threadIdx.x >> 3;
-  const int c0 = blockIdx.x * 64 + cc * 8;
+  __shared__ float ps[CR_RG][CR_COLS + 1], q[8 * (CR_COLS + 1)];
+  const int cc = threadIdx.x & 3, rg = threadIdx.x >> 2;
+  const int c0 = blockIdx.x * CR_COLS + cc * 8;
   float s[8] = {};
   if (c0 < N) {
-    for (int t = rg; t < n; t += 32) {
-      float v[8];
-      load8(A + (long)t * lda + c0, v);
+    for (int t0 = rg; t0 < n; t0 += CR_UNROLL * CR_RG) {
+      float v[CR_UNROLL][8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) s[e] += v[e];
+      for (int k = 0; k < CR_UNROLL; ++k)
+        if (t0 + k * CR_RG < n) load8(A + (long)(t0 + k * CR_RG) * lda + c0, v[k]);
+#pragma unroll
+      for (int k = 0; k < CR_UNROLL; ++k)
+        if (t0 + k * CR_RG < n)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) s[e] += v[k][e];
     }
   }
 #pragma unroll
   for (int e = 0; e < 8; ++e) ps[rg][cc * 8 + e] = s[e];
   __syncthreads();
-  if (threadIdx.x < 64) {
-    const int col = blockIdx.x * 64 + threadIdx.x;
-    if (col < N) {
-      float a = 0.f;
-      for (int r = 0; r < 32; ++r) a += ps[r][threadIdx.x];
-      out[col] += a;
-    }
-  }
+  const float a = col_partials_sum(ps, q);
+  const int col = blockIdx.x * CR_COLS + threadIdx.x;
+  if (threadIdx.x < CR_COLS && col < N) out[col] += a;
 }
 
+// dK and dV (fp32, [n, H]) into the K and V thirds of the dQKV rows, 8
+// consecutive columns per thread (H % 8 == 0; 16-byte aligned pointers).
 template <typename T>
 __global__ void pack_dkv_kernel(int n, int H, const float* dk, const float* dv, T* dqkv) {
+  const int h8 = H >> 3;
   const long e = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= (long)n * H) return;
-  const long i = e / H, j = e % H;
-  st(dqkv + i * 3 * H + H + j, dk[e]);
-  st(dqkv + i * 3 * H + 2 * H + j, dv[e]);
+  if (e >= (long)n * h8) return;
+  const long i = e / h8, j = (e - i * h8) * 8;
+  float v[8];
+  load8(dk + i * H + j, v);
+  store8(dqkv + i * 3 * H + H + j, v);
+  load8(dv + i * H + j, v);
+  store8(dqkv + i * 3 * H + 2 * H + j, v);
 }
 
 __global__ void fill_f32_kernel(float* p, size_t n, float v) {
@@ -447,24 +505,32 @@ __global__ void copy_kernel(size_t n, const T* src, T* dst) {
 hipError_t ln_fwd(int dtype, int n, int H, const void* x, void* x_copy, const void* g,
                   const void* b, void* u, float* mean, float* rstd, float eps, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  if (dtype == DT_FP32)
-    ln_fwd_kernel<float><<<n, 256, 0, s>>>(H, (const float*)x, (float*)x_copy, (const float*)g,
-                                           (const float*)b, (float*)u, mean, rstd, eps);
-  else
-    ln_fwd_kernel<bf16><<<n, 256, 0, s>>>(H, (const bf16*)x, (bf16*)x_copy, (const bf16*)g,
-                                          (const bf16*)b, (bf16*)u, mean, rstd, eps);
+  const LnShape sh = ln_shape(H);
+#define TP_LN(TT, C)                                                                        \
+  ln_fwd_kernel<TT, C><<<n, sh.nt, 0, s>>>(H, (const TT*)x, (TT*)x_copy, (const TT*)g,      \
+                                           (const TT*)b, (TT*)u, mean, rstd, eps)
+  if (dtype == DT_FP32) {
+    if (sh.cpt == 1) TP_LN(float, 1); else TP_LN(float, 2);
+  } else {
+    if (sh.cpt == 1) TP_LN(bf16, 1); else TP_LN(bf16, 2);
+  }
+#undef TP_LN
   return hipGetLastError();
 }
 
 hipError_t ln_bwd(int dtype, int n, int H, const void* du, const void* x, const float* mean,
                   const float* rstd, const void* g, const void* resid, void* dx, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  if (dtype == DT_FP32)
-    ln_bwd_kernel<float><<<n, 256, 0, s>>>(H, (const float*)du, (const float*)x, mean, rstd,
-                                           (const float*)g, (const float*)resid, (float*)dx);
-  else
-    ln_bwd_kernel<bf16><<<n, 256, 0, s>>>(H, (const bf16*)du, (const bf16*)x, mean, rstd,
-                                          (const bf16*)g, (const bf16*)resid, (bf16*)dx);
+  const LnShape sh = ln_shape(H);
+#define TP_LN(TT, C)                                                                        \
+  ln_bwd_kernel<TT, C><<<n, sh.nt, 0, s>>>(H, (const TT*)du, (const TT*)x, mean, rstd,      \
+                                           (const TT*)g, (const TT*)resid, (TT*)dx)
+  if (dtype == DT_FP32) {
+    if (sh.cpt == 1) TP_LN(float, 1); else TP_LN(float, 2);
+  } else {
+    if (sh.cpt == 1) TP_LN(bf16, 1); else TP_LN(bf16, 2);
+  }
+#undef TP_LN
   return hipGetLastError();
 }
 
@@ -472,29 +538,33 @@ hipError_t ln_param_grads(int dtype, int n, int H, const void* du, const void* x
                           const float* mean, const float* rstd, float* dg, float* db,
                           hipStream_t s) {
   if (n <= 0) return hipSuccess;
+  const int blocks = cdiv(H, CR_COLS);
   if (dtype == DT_FP32)
-    ln_param_grads_kernel<float><<<cdiv(H, 64), 256, 0, s>>>(n, H, (const float*)du,
-                                                               (const float*)x, mean, rstd, dg, db);
+    ln_param_grads_kernel<float><<<blocks, 256, 0, s>>>(n, H, (const float*)du, (const float*)x,
+                                                        mean, rstd, dg, db);
   else
-    ln_param_grads_kernel<bf16><<<cdiv(H, 64), 256, 0, s>>>(n, H, (const bf16*)du,
-                                                              (const bf16*)x, mean, rstd, dg, db);
+    ln_param_grads_kernel<bf16><<<blocks, 256, 0, s>>>(n, H, (const bf16*)du, (const bf16*)x,
+                                                       mean, rstd, dg, db);
   return hipGetLastError();
 }
 
 hipError_t colsum_acc(int dtype, int n, int N, const void* A, long lda, float* out,
                       hipStream_t s) {
   if (n <= 0 || N <= 0) return hipSuccess;
+  const int blocks = cdiv(N, CR_COLS);
   if (dtype == DT_FP32)
-    colsum_kernel<float><<<cdiv(N, 64), 256, 0, s>>>(n, N, (const float*)A, lda, out);
+    colsum_kernel<float><<<blocks, 256, 0, s>>>(n, N, (const float*)A, lda, out);
   else
-    colsum_kernel<bf16><<<cdiv(N, 64), 256, 0, s>>>(n, N, (const bf16*)A, lda, out);
+    colsum_kernel<bf16><<<blocks, 256, 0, s>>>(n, N, (const bf16*)A, lda, out);
   return hipGetLastError();
 }
 
 hipError_t pack_dkv(int dtype, int n, int H, const float* dk, const float* dv, void* dqkv,
                     hipStream_t s) {
-  const long tot = (long)n * H;
+  const long tot = (long)n * (H / 8);
   if (tot <= 0) return hipSuccess;
+  auto al = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
+  if (H % 8 || !al(dk) || !al(dv) || !al(dqkv)) return hipErrorInvalidValue;
   if (dtype == DT_FP32)
     pack_dkv_kernel<float><<<cdiv(tot, 256), 256, 0, s>>>(n, H, dk, dv, (float*)dqkv);
   else
