@@ -303,8 +303,10 @@ __global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma
   const uint32_t sbase = lds_addr(smem);
 
   // K fragments of the wave's keys stay in registers; V fragments (dK needs
-  // them for dP) are reloaded from L2 per query block in the dK-only mode
-  constexpr bool V_RESIDENT = MODE == 0;
+  // them for dP) too in mode 0, while the dK-only mode keeps the block's V
+  // rows in LDS (loaded once, after the query-tile ring) and reads them per
+  // query block
+  constexpr bool V_RESIDENT = MODE == 0, V_LDS = MODE == 2;
   u32x4 kf[KS], vf[KS];
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) {
@@ -333,7 +335,13 @@ __global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma
     const int tq = min(a.l + i0 + (lane & 31), a.Lmax - 1);
     dma4((lane < 32 ? lse_h : D_h) + tq, st + 2 * TILE + w * 128);
   };
-  if (nqb > 0) issue(0, 0);
+  const uint32_t Vl = sbase + ST * STAGE * 2;  // V rows of the block's keys (V_LDS)
+  if (nqb > 0) {
+    if constexpr (V_LDS)
+      T::template dma<32 * NW, NTH>(Vc + (long)k_lo * H, H, min(32 * NW, a.r - k_lo),
+                                    smem + ST * STAGE);
+    issue(0, 0);
+  }
   for (int qb = 0; qb < nqb; ++qb) {
     wait_vm<0>();
     __builtin_amdgcn_s_barrier();
@@ -346,10 +354,7 @@ __global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma
       const uint32_t LD = Qt + 2 * TILE * 2 + w * 256;
       u32x4 lq[4], dq4[4];
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        lq[b] = ds_read128(LD + (8 * b + 4 * G) * 4);
-        if constexpr (DO_K) dq4[b] = ds_read128(LD + 128 + (8 * b + 4 * G) * 4);
-      }
+      for (int b = 0; b < 4; ++b) lq[b] = ds_read128(LD + (8 * b + 4 * G) * 4);
       f32x16_t s = zero16(), dp = zero16();
       {
         u32x4 qa[KS];
@@ -359,12 +364,23 @@ __global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma
 #pragma unroll
         for (int kk = 1; kk < KS; ++kk) lgkm_tie(qa[kk]);
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          lgkm_tie(lq[b]);
-          if constexpr (DO_K) lgkm_tie(dq4[b]);
-        }
+        for (int b = 0; b < 4; ++b) lgkm_tie(lq[b]);
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) s = mfma(qa[kk], kf[kk], s);
+      }
+      // s[v]: query row qi = 8 (v / 4) + 4 G + v % 4 of the block, key s_me.
+      // P first, so the lse values are dead before the dP product.
+      f32x16_t p, ds;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int qi = 8 * (v >> 2) + 4 * G + (v & 3);
+        const bool ok = qi < qval && s_me <= a.l + i0 + qi;
+        const float lse_q = __uint_as_float(lq[v >> 2][v & 3]);
+        p[v] = ok ? exp2_fast(__builtin_fmaf(s[v], sl2, -lse_q * LOG2E)) : 0.f;
+      }
+      if constexpr (DO_K) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b) dq4[b] = ds_read128(LD + 128 + (8 * b + 4 * G) * 4);
       }
       if constexpr (DO_K && V_RESIDENT) {
         u32x4 oa[KS];
@@ -374,37 +390,37 @@ __global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma
 #pragma unroll
         for (int kk = 1; kk < KS; ++kk) lgkm_tie(oa[kk]);
 #pragma unroll
+        for (int b = 0; b < 4; ++b) lgkm_tie(dq4[b]);
+#pragma unroll
         for (int kk = 0; kk < KS; ++kk) dp = mfma(oa[kk], vf[kk], dp);
       } else if constexpr (DO_K) {
-        // dP = dO V^T in two halves of the head width, V rows from L2
+        // dP = dO V^T in two halves of the head width, V rows from LDS (rows
+        // of keys >= r repeat the last key; their scores are masked)
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf) {
           u32x4 oa[KS / 2], vr[KS / 2];
 #pragma unroll
           for (int kk = 0; kk < KS / 2; ++kk) {
             const int k2 = hf * (KS / 2) + kk;
-            vr[kk] = s_me < a.r ? *(const u32x4*)(Vc + (long)s_me * H + 16 * k2 + 8 * G)
-                                : u32x4{0, 0, 0, 0};
+            vr[kk] = T::row8(Vl, 32 * w + c, 2 * k2 + G);
             oa[kk] = T::row8(Ot, c, 2 * k2 + G);
           }
-          lgkm_wait(oa[0]);
+          lgkm_wait(vr[0]);
 #pragma unroll
-          for (int kk = 1; kk < KS / 2; ++kk) lgkm_tie(oa[kk]);
+          for (int kk = 1; kk < KS / 2; ++kk) lgkm_tie(vr[kk]);
+#pragma unroll
+          for (int kk = 0; kk < KS / 2; ++kk) lgkm_tie(oa[kk]);
+          if (hf == 0) {
+#pragma unroll
+            for (int b = 0; b < 4; ++b) lgkm_tie(dq4[b]);
+          }
 #pragma unroll
           for (int kk = 0; kk < KS / 2; ++kk) dp = mfma(oa[kk], vr[kk], dp);
         }
       }
-      // s[v], dp[v]: query row qi = 8 (v / 4) + 4 G + v % 4 of the block, key s_me
-      f32x16_t p, ds;
+      if constexpr (DO_K) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int qi = 8 * (v >> 2) + 4 * G + (v & 3);
-        const int tq = a.l + i0 + qi;
-        const bool ok = qi < qval && s_me <= tq;
-        const float lse_q = __uint_as_float(lq[v >> 2][v & 3]);
-        const float pv = ok ? exp2_fast(__builtin_fmaf(s[v], sl2, -lse_q * LOG2E)) : 0.f;
-        p[v] = pv;
-        if constexpr (DO_K) ds[v] = pv * (dp[v] - __uint_as_float(dq4[v >> 2][v & 3]));
+        for (int v = 0; v < 16; ++v) ds[v] = p[v] * (dp[v] - __uint_as_float(dq4[v >> 2][v & 3]));
       }
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
@@ -628,12 +644,15 @@ hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   constexpr size_t lds_kv = 2 * (2 * 32 * D + NWF * 128) * 2;
+  constexpr size_t lds_kv_v = lds_kv + 32 * NWF * D * 2;  // + the block's V rows
   const dim3 grid_kv(cdiv(a.r, 32 * NWF), a.heads);
   attn_bwd_dkdv_mfma<D, NWF, DKDV_MODE_A><<<grid_kv, 64 * NWF, lds_kv, s>>>(a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if constexpr (DKDV_MODE_A != 0) {
-    attn_bwd_dkdv_mfma<D, NWF, 2><<<grid_kv, 64 * NWF, lds_kv, s>>>(a);
+    e = set_lds(attn_bwd_dkdv_mfma<D, NWF, 2>, lds_kv_v);
+    if (e != hipSuccess) return e;
+    attn_bwd_dkdv_mfma<D, NWF, 2><<<grid_kv, 64 * NWF, lds_kv_v, s>>>(a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
