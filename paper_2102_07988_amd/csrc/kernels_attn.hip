@@ -62,6 +62,27 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
 // a softmax weight may do).
 __device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// IEEE maximum (NaN-propagating; v_maximum3_f32 needs no operand
+// canonicalisation, unlike fmaxf).
+__device__ inline float fmax_ieee(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
+// Lanes l and l ^ 32 combined: after v_permlane32_swap every lane holds the
+// lower half's value in .x and the upper half's in .y, so both lanes of a pair
+// compute op(lower, upper) and get the same result.
+__device__ inline float2 halves(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return make_float2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float pair_max(float v) {
+  const float2 h = halves(v);
+  return fmax_ieee(h.x, h.y);
+}
+__device__ inline float pair_sum(float v) {
+  const float2 h = halves(v);
+  return h.x + h.y;
+}
+
 // 8 accumulator values (one reduction half) as a bf16 operand.
 __device__ inline u32x4 acc_half_bf16(const f32x16_t& x, int ks) {
   u32x4 u;
@@ -99,13 +120,40 @@ struct Tile {
     const u32x2 hi = ds_read_tr(base + off(r + 8, col >> 3) + inchunk);
     return join(lo, hi);
   }
+  // DMA of full ROWS-row tiles with this thread's chunk offsets (bytes from
+  // the tile's first row, rows of ld elements) computed once, so a tile only
+  // moves the wave-uniform origin; a tile with fewer valid rows takes `dma`.
+  template <int ROWS, int NTH>
+  struct Dma {
+    static constexpr int CH = ROWS * CPR / NTH;
+    uint32_t off[CH];
+    int w;  // wave index, wave-uniform
+    __device__ Dma(long ld, int wave) : w(wave) {
+      const int lane = threadIdx.x & 63;
+#pragma unroll
+      for (int i = 0; i < CH; ++i) {
+        const int s = i * NTH + w * 64 + lane;
+        const int r = s / CPR, c = (s % CPR) ^ f(r);
+        off[i] = (uint32_t)(((long)r * ld + c * 8) * 2);
+      }
+    }
+    __device__ void issue(const uint16_t* G, long ld, int rvalid, uint16_t* lds) const {
+      if (rvalid >= ROWS) {
+#pragma unroll
+        for (int i = 0; i < CH; ++i)
+          dma16((const char*)G + off[i], lds + (i * NTH + w * 64) * 8);
+      } else {
+        dma<ROWS, NTH>(G, ld, rvalid, lds);
+      }
+    }
+  };
   // DMA rows [0, ROWS) of a global [token][*] block (row stride ld elements);
   // rows >= rvalid repeat row rvalid - 1 (their products are masked).
   template <int ROWS, int NTH>
   __device__ static void dma(const uint16_t* G, long ld, int rvalid, uint16_t* lds) {
     constexpr int CH = ROWS * CPR / NTH;
     static_assert(CH * NTH == ROWS * CPR, "uneven tile DMA");
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
       const int s = i * NTH + w * 64 + lane;
@@ -159,11 +207,12 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a) {
   for (int j = 0; j < JB; ++j) o[j] = zero16();
 
   const int nkb = (kend_blk + BKV - 1) / BKV;
+  const typename T::template Dma<BKV, NTH> kvd(H, __builtin_amdgcn_readfirstlane(w));
   auto issue = [&](int stage, int kb) {
     uint16_t* st = smem + stage * STAGE;
     const int rv = min(BKV, kend_blk - kb * BKV);
-    T::template dma<BKV, NTH>(Kc + (long)kb * BKV * H, H, rv, st);
-    T::template dma<BKV, NTH>(Vc + (long)kb * BKV * H, H, rv, st + TILE);
+    kvd.issue(Kc + (long)kb * BKV * H, H, rv, st);
+    kvd.issue(Vc + (long)kb * BKV * H, H, rv, st + TILE);
   };
   issue(0, 0);
   for (int kb = 0; kb < nkb; ++kb) {
@@ -176,16 +225,19 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a) {
       f32x16_t p[2];  // raw scores, -inf where masked
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb) {
-        f32x16_t s = zero16();
-        if (kbase + 32 * sb < kend_w) {
+        // computed also for a sub-block past the wave's last query (its rows
+        // exist in the tile; every such score is masked below)
+        f32x16_t s;
+        {
           u32x4 kf[KS];
 #pragma unroll
           for (int kk = 0; kk < KS; ++kk) kf[kk] = T::row8(Kt, 32 * sb + c, 2 * kk + G);
           lgkm_wait(kf[0]);
 #pragma unroll
           for (int kk = 1; kk < KS; ++kk) lgkm_tie(kf[kk]);
+          s = mfma(kf[0], qf[0], zero16());
 #pragma unroll
-          for (int kk = 0; kk < KS; ++kk) s = mfma(kf[kk], qf[kk], s);
+          for (int kk = 1; kk < KS; ++kk) s = mfma(kf[kk], qf[kk], s);
         }
         // keys of a sub-block that ends at or before the wave's first query
         // need no mask (all are <= every query of the wave and < r)
@@ -201,8 +253,8 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a) {
       }
       float mx = -INFINITY;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, fmaxf(p[0][v], p[1][v]));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * sl2;
+      for (int v = 0; v < 16; ++v) mx = fmax_ieee(mx, fmax_ieee(p[0][v], p[1][v]));
+      mx = pair_max(mx) * sl2;
       if (__builtin_amdgcn_ballot_w64(mx > m + RESCALE_LOG2) != 0) {  // wave-uniform
         const float mnew = fmaxf(m, mx);
         // no visible key yet for this query (both stay -inf): nothing to scale
@@ -226,8 +278,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a) {
           p[sb][v] = e;
           rs += e;
         }
-      rs += __shfl_xor(rs, 32, 64);
-      lsum += rs;
+      lsum += pair_sum(rs);
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb) {
         if (kbase + 32 * sb >= kend_w) break;
@@ -283,13 +334,16 @@ __global__ __launch_bounds__(256) void attn_bwd_rowdot(AttnArgs a) {
 // MODE 0: dK and dV; 1: dV only (S, P, dV += P^T dO); 2: dK only (S, dP, dS,
 // dK += dS^T Q).  The single-output modes hold one accumulator set and fit
 // two waves per SIMD; together they recompute S once more than mode 0.
-template <int D, int NW, int MODE>
+// ST query tiles form the LDS ring: tile qb + ST - 1 is requested while tile
+// qb is multiplied.
+template <int D, int NW, int MODE, int ST>
 __global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma(AttnArgs a) {
   using T = Tile<D>;
   constexpr bool DO_K = MODE != 1, DO_V = MODE != 2;
-  constexpr int NTH = 64 * NW, BQ = 32, KS = D / 16, JB = D / 32, ST = 2;
+  constexpr int NTH = 64 * NW, BQ = 32, KS = D / 16, JB = D / 32;
   constexpr int TILE = BQ * D;                           // elements
   constexpr int STAGE = 2 * TILE + NW * 128;             // Q, dO, then per-wave [lse | D]
+  constexpr int PER_ISSUE = 2 * (BQ * D / 8) / NTH + 1;  // DMA instructions per tile
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   const int h = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int G = lane >> 5, c = lane & 31, H = a.H;
@@ -326,11 +380,12 @@ __global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma
   const int nqb = (n - i_begin + BQ - 1) / BQ;
   const float* lse_h = a.lse + (long)h * a.Lmax;
   const float* D_h = a.D + (long)h * a.Lmax;
+  const typename T::template Dma<BQ, NTH> qd(H, __builtin_amdgcn_readfirstlane(w));
   auto issue = [&](int stage, int qb) {
     uint16_t* st = smem + stage * STAGE;
     const int i0 = i_begin + qb * BQ, qv = min(BQ, n - i0);
-    T::template dma<BQ, NTH>(Q + (long)i0 * H, H, qv, st);
-    T::template dma<BQ, NTH>(dO + (long)i0 * H, H, qv, st + TILE);
+    qd.issue(Q + (long)i0 * H, H, qv, st);
+    qd.issue(dO + (long)i0 * H, H, qv, st + TILE);
     // per-wave copy of lse (lanes 0..31) and D (lanes 32..63) of the block's queries
     const int tq = min(a.l + i0 + (lane & 31), a.Lmax - 1);
     dma4((lane < 32 ? lse_h : D_h) + tq, st + 2 * TILE + w * 128);
@@ -340,12 +395,14 @@ __global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma
     if constexpr (V_LDS)
       T::template dma<32 * NW, NTH>(Vc + (long)k_lo * H, H, min(32 * NW, a.r - k_lo),
                                     smem + ST * STAGE);
-    issue(0, 0);
+    for (int i = 0; i < ST - 1 && i < nqb; ++i) issue(i, i);
   }
   for (int qb = 0; qb < nqb; ++qb) {
-    wait_vm<0>();
+    // tile qb has landed once at most the ST - 2 later tiles are in flight
+    if (qb + ST - 1 <= nqb) wait_vm<(ST - 2) * PER_ISSUE>();
+    else wait_vm<0>();
     __builtin_amdgcn_s_barrier();
-    if (qb + 1 < nqb) issue((qb + 1) % ST, qb + 1);
+    if (qb + ST - 1 < nqb) issue((qb + ST - 1) % ST, qb + ST - 1);
     const int i0 = i_begin + qb * BQ, qval = min(BQ, n - i0);
     // the wave's keys [s_w, s_w + 32) meet queries up to l + i0 + qval - 1
     if (s_w <= a.l + i0 + qval - 1 && s_w < a.r) {
@@ -538,11 +595,12 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a) {
   for (int j = 0; j < JB; ++j) dq[j] = zero16();
 
   const int nkb = (kend_blk + BKV - 1) / BKV;
+  const typename T::template Dma<BKV, NTH> kvd(H, __builtin_amdgcn_readfirstlane(w));
   auto issue = [&](int stage, int kb) {
     uint16_t* st = smem + stage * STAGE;
     const int rv = min(BKV, kend_blk - kb * BKV);
-    T::template dma<BKV, NTH>(Kc + (long)kb * BKV * H, H, rv, st);
-    T::template dma<BKV, NTH>(Vc + (long)kb * BKV * H, H, rv, st + TILE);
+    kvd.issue(Kc + (long)kb * BKV * H, H, rv, st);
+    kvd.issue(Vc + (long)kb * BKV * H, H, rv, st + TILE);
   };
   issue(0, 0);
   for (int kb = 0; kb < nkb; ++kb) {
@@ -643,16 +701,25 @@ hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
   attn_bwd_rowdot<D><<<cdiv((long)n * a.heads, 4), 256, 0, s>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  constexpr size_t lds_kv = 2 * (2 * 32 * D + NWF * 128) * 2;
-  constexpr size_t lds_kv_v = lds_kv + 32 * NWF * D * 2;  // + the block's V rows
-  const dim3 grid_kv(cdiv(a.r, 32 * NWF), a.heads);
-  attn_bwd_dkdv_mfma<D, NWF, DKDV_MODE_A><<<grid_kv, 64 * NWF, lds_kv, s>>>(a);
+  // dV kernel: 4 waves, a 4-tile ring (69 KB, two blocks per CU).  dK kernel:
+  // the block's V rows stay in LDS; with head width 128 it runs 8 waves (256
+  // keys) over a 4-tile ring (137 KB, one block per CU), with 64 4 waves over
+  // a 2-tile ring.
+  constexpr int STA = DKDV_MODE_A == 0 ? 2 : 4;
+  constexpr int NWK = D == 128 ? 8 : 4, STK = D == 128 ? 4 : 2;
+  constexpr size_t lds_a = STA * (2 * 32 * D + NWF * 128) * 2;
+  constexpr size_t lds_k = STK * (2 * 32 * D + NWK * 128) * 2 + 32 * NWK * D * 2;
+  e = set_lds(attn_bwd_dkdv_mfma<D, NWF, DKDV_MODE_A, STA>, lds_a);
+  if (e != hipSuccess) return e;
+  attn_bwd_dkdv_mfma<D, NWF, DKDV_MODE_A, STA>
+      <<<dim3(cdiv(a.r, 32 * NWF), a.heads), 64 * NWF, lds_a, s>>>(a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if constexpr (DKDV_MODE_A != 0) {
-    e = set_lds(attn_bwd_dkdv_mfma<D, NWF, 2>, lds_kv_v);
+    e = set_lds(attn_bwd_dkdv_mfma<D, NWK, 2, STK>, lds_k);
     if (e != hipSuccess) return e;
-    attn_bwd_dkdv_mfma<D, NWF, 2><<<grid_kv, 64 * NWF, lds_kv_v, s>>>(a);
+    attn_bwd_dkdv_mfma<D, NWK, 2, STK>
+        <<<dim3(cdiv(a.r, 32 * NWK), a.heads), 64 * NWK, lds_k, s>>>(a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
