@@ -427,13 +427,23 @@ __global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma
       }
       // s[v]: query row qi = 8 (v / 4) + 4 G + v % 4 of the block, key s_me.
       // P first, so the lse values are dead before the dP product.
+      // A full query block whose first query follows every key of the wave
+      // needs no mask.
       f32x16_t p, ds;
+      if (qval == BQ && s_w + 31 <= a.l + i0) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int qi = 8 * (v >> 2) + 4 * G + (v & 3);
-        const bool ok = qi < qval && s_me <= a.l + i0 + qi;
-        const float lse_q = __uint_as_float(lq[v >> 2][v & 3]);
-        p[v] = ok ? exp2_fast(__builtin_fmaf(s[v], sl2, -lse_q * LOG2E)) : 0.f;
+        for (int v = 0; v < 16; ++v) {
+          const float lse_q = __uint_as_float(lq[v >> 2][v & 3]);
+          p[v] = exp2_fast(__builtin_fmaf(s[v], sl2, -lse_q * LOG2E));
+        }
+      } else {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int qi = 8 * (v >> 2) + 4 * G + (v & 3);
+          const bool ok = qi < qval && s_me <= a.l + i0 + qi;
+          const float lse_q = __uint_as_float(lq[v >> 2][v & 3]);
+          p[v] = ok ? exp2_fast(__builtin_fmaf(s[v], sl2, -lse_q * LOG2E)) : 0.f;
+        }
       }
       if constexpr (DO_K) {
 #pragma unroll
@@ -635,13 +645,21 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a) {
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) dp = mfma(va[kk], of[kk], dp);
       }
+      // keys of a sub-block that ends at or before the wave's first query,
+      // with all 32 queries of the wave valid, need no mask
       f32x16_t ds;
+      if (kbase + 32 * sb + 31 <= q_lo + 32 * w && q_lo + 32 * w + 32 <= a.r) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int key = kbase + 32 * sb + 8 * (v >> 2) + 4 * G + (v & 3);
-        const bool ok = tvalid && key <= t;
-        const float pv = ok ? exp2_fast(__builtin_fmaf(s[v], sl2, -lse2)) : 0.f;
-        ds[v] = pv * (dp[v] - Dt);
+        for (int v = 0; v < 16; ++v)
+          ds[v] = exp2_fast(__builtin_fmaf(s[v], sl2, -lse2)) * (dp[v] - Dt);
+      } else {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int key = kbase + 32 * sb + 8 * (v >> 2) + 4 * G + (v & 3);
+          const bool ok = tvalid && key <= t;
+          const float pv = ok ? exp2_fast(__builtin_fmaf(s[v], sl2, -lse2)) : 0.f;
+          ds[v] = pv * (dp[v] - Dt);
+        }
       }
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
