@@ -71,6 +71,10 @@ typedef struct {
   int dtype;      /* tp_dtype */
   int wgrad_mode; /* tp_wgrad_mode */
   float ln_eps;   /* LayerNorm epsilon (1e-5 in the GPT-3 setting) */
+  int batch;      /* b: sequences that move through the stage together as one batch slice
+                     (Sec. 3.4, slicing the batch and token dimensions jointly); 0 means 1,
+                     at most 64.  Token t of sequence s is row t * b + s of every
+                     slice tensor below, so a slice [l, r) is (r-l) * b consecutive rows. */
 } tp_stage_config;
 
 /* Parameters (stage dtype) or gradients (fp32) of one layer.  Shapes:
@@ -110,8 +114,8 @@ void tp_stage_destroy(tp_stage *stage);
 tp_status tp_kv_prefix_reset(tp_stage *stage);
 
 /* Forward of token slice [l, r) through every layer (Sec. 3.2).
- * x: [r-l][H] stage input rows, y: [r-l][H] stage output rows (stage dtype,
- * device).  Requires 0 <= l < r <= max_seq (else TP_ERR_INVALID) and l equal to
+ * x: [r-l][b][H] stage input rows, y: [r-l][b][H] stage output rows (stage
+ * dtype, device; b = cfg.batch, token-major).  Requires 0 <= l < r <= max_seq (else TP_ERR_INVALID) and l equal to
  * the number of cached tokens (else TP_ERR_ORDER).  Appends the slice's keys
  * and values to each layer's cache, saves what backward needs, and sets the
  * cached length and the backward frontier to r.  x and y must not overlap and
@@ -119,8 +123,8 @@ tp_status tp_kv_prefix_reset(tp_stage *stage);
 tp_status tp_slice_forward(tp_stage *stage, int l, int r, const void *x, void *y);
 
 /* Backward of token slice [l, r) through every layer, in reverse layer order.
- * dy: [r-l][H] gradient of the stage output rows, dx: [r-l][H] gradient of the
- * stage input rows (stage dtype, device).  Requires 0 <= l < r and r equal to
+ * dy: [r-l][b][H] gradient of the stage output rows, dx: [r-l][b][H] gradient
+ * of the stage input rows (stage dtype, device).  Requires 0 <= l < r and r equal to
  * the backward frontier (slices arrive in reverse order; their boundaries need
  * not match the forward slicing), else TP_ERR_ORDER / TP_ERR_INVALID.  Adds
  * this slice's contributions to the parameter gradients; the gradient that
@@ -158,6 +162,33 @@ tp_status tp_profile_slice_cost(tp_stage *stage, const int *lens, int n_lens, co
  * K < 1, eps_ns < 0, a negative cost among the used entries). */
 tp_status tp_dp_optimal_slicing(const int64_t *cost, int L_units, int unit, int K, int64_t eps_ns,
                                 int *out_lens, int *out_M, int64_t *out_T);
+
+/* Batch split of Sec. 3.4 (slicing the batch and token dimensions jointly):
+ * a batch of B sequences is cut into groups of b_1 + ... + b_D = B sequences,
+ * each group pipelined with its own optimal token slicing, minimising
+ * T_{b_1} + ... + T_{b_D} (a one-dimensional knapsack).  T_b (host, int64,
+ * [B]): T_b[b-1] = the optimal latency of a group of b sequences (e.g. *out_T
+ * of tp_dp_optimal_slicing on the cost table of a stage with batch b); a
+ * negative entry marks a size that may not be used.  Outputs: out_sizes (capacity
+ * B) the group sizes, largest first, *out_D their number, *out_total the
+ * minimal sum.  Ties: for each prefix total the last group is the smallest
+ * size reaching the minimum.  Host only, deterministic.  Errors:
+ * TP_ERR_INVALID (null pointer, B < 1, no combination of usable sizes sums
+ * to B, overflow). */
+tp_status tp_dp_batch_split(const int64_t *T_b, int B, int *out_sizes, int *out_D,
+                            int64_t *out_total);
+
+/* Joint plan of Sec. 3.4: tp_dp_optimal_slicing on the cost table of every
+ * group size b = 1..B, then tp_dp_batch_split over the resulting latencies.
+ * costs (host, int64, [B][L_units][L_units]): plane b-1 is the table of a batch
+ * slice of b sequences, in the layout of tp_dp_optimal_slicing.  Outputs:
+ * out_T_b[B] the latency of each size; out_sizes / *out_D / *out_total as
+ * tp_dp_batch_split; for group g, out_M[g] slices with token lengths
+ * out_lens[g * L_units .. g * L_units + out_M[g]) (capacities: out_sizes,
+ * out_M: B; out_lens: B * L_units).  Errors: those of the two calls. */
+tp_status tp_dp_joint_slicing(const int64_t *costs, int B, int L_units, int unit, int K,
+                              int64_t eps_ns, int *out_sizes, int *out_D, int *out_lens,
+                              int *out_M, int64_t *out_T_b, int64_t *out_total);
 
 /* Cost estimate of Sec. 3.3 (Eq. 9): t(i, j) = t(i, 0) + t_ctx(i, j) with the
  * context overhead t_ctx(i, j) = a0 + a1 i + a2 j + a3 i j (i = slice length,

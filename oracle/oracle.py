@@ -1,7 +1,7 @@
 """ctypes front end of the fp64 CPU oracle -- TEST INFRASTRUCTURE ONLY.
 
 What is computed is defined in tp_oracle.c (stage forward/backward over token
-slices and Algorithm 1 of the paper).  This module adds three plain-Python
+slices and Algorithm 1 of the paper).  This module adds plain-Python
 pieces that need no speed:
 
 * ``eq5_latency`` -- the pipeline latency of a slicing, Eq. 5:
@@ -11,6 +11,9 @@ pieces that need no speed:
 * ``slice_flops`` / ``paper_tflops_per_gpu`` -- the arithmetic a slice of a
   pre-LN block must do, and the per-GPU TFLOP/s convention of the paper's
   result tables (Tables 2-4 in the appendix).
+* ``batch_split`` / ``exhaustive_batch_split`` / ``joint_slicing`` -- the
+  batch dimension of Sec. 3.4: groups of sequences, each token-sliced, sizes
+  chosen by a one-dimensional knapsack over the per-size latencies.
 * ``fit_ctx_model`` / ``cost_table_from_model`` -- the cost estimate of
   Sec. 3.3 (Eq. 9): t(i, j) = t(i, 0) + t_ctx(i, j) with the context overhead
   t_ctx = a0 + a1 i + a2 j + a3 i j fitted by least squares.
@@ -238,6 +241,73 @@ def dp_optimal_slicing(cost: np.ndarray, K: int, eps: int = 0):
     if rc != 0:
         raise ValueError(f"oracle DP rejected its arguments ({rc})")
     return [out[i] for i in range(M.value)], T.value, tmax.value, ev.value
+
+
+# ------------------------------------------------------ batch split (Sec. 3.4)
+
+def batch_split(T_b: Sequence[int]) -> Tuple[List[int], int]:
+    """Sec. 3.4: cut a batch of B = len(T_b) sequences into groups b_1..b_D
+    (sum B) minimising T_{b_1} + ... + T_{b_D}, T_b = T_b[b-1] the optimal
+    latency of a group of b sequences (negative: unusable).  The knapsack
+    recurrence best[x] = min_b best[x - b] + T_b, b ascending, replaced only on
+    a strictly smaller total.  Returns (sizes largest first, total)."""
+    B = len(T_b)
+    INF = None
+    best = [0] + [INF] * B
+    last = [0] * (B + 1)
+    for x in range(1, B + 1):
+        for b in range(1, x + 1):
+            t = int(T_b[b - 1])
+            if t < 0 or best[x - b] is INF:
+                continue
+            v = best[x - b] + t
+            if best[x] is INF or v < best[x]:
+                best[x], last[x] = v, b
+    if best[B] is INF:
+        raise ValueError("no combination of usable group sizes sums to B")
+    sizes, x = [], B
+    while x > 0:
+        sizes.append(last[x])
+        x -= last[x]
+    return sorted(sizes, reverse=True), best[B]
+
+
+def integer_partitions(B: int, largest: int = None):
+    """Every multiset of positive integers summing to B, as non-increasing tuples."""
+    largest = B if largest is None else largest
+    if B == 0:
+        yield ()
+        return
+    for first in range(min(B, largest), 0, -1):
+        for rest in integer_partitions(B - first, first):
+            yield (first,) + rest
+
+
+def exhaustive_batch_split(T_b: Sequence[int]) -> Tuple[int, List[Tuple[int, ...]]]:
+    """Brute force over all partitions of B: the minimal sum and every argmin."""
+    best, arg = None, []
+    for part in integer_partitions(len(T_b)):
+        if any(T_b[b - 1] < 0 for b in part):
+            continue
+        v = sum(int(T_b[b - 1]) for b in part)
+        if best is None or v < best:
+            best, arg = v, [part]
+        elif v == best:
+            arg.append(part)
+    return best, arg
+
+
+def joint_slicing(costs: np.ndarray, K: int, eps: int = 0):
+    """Sec. 3.4 joint plan on [B][U][U] tables (plane b-1: a group of b
+    sequences): the token DP per group size, then the batch split.  Returns
+    (groups [(b, units)], T_b list, total)."""
+    T_b, units = [], []
+    for b in range(costs.shape[0]):
+        u, T, _, _ = dp_optimal_slicing(costs[b], K, eps)
+        T_b.append(T)
+        units.append(u)
+    sizes, total = batch_split(T_b)
+    return [(b, units[b - 1]) for b in sizes], T_b, total
 
 
 # ------------------------------------------------------------------ flop counts

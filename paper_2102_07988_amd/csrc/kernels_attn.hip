@@ -170,13 +170,14 @@ struct Tile {
 // two waves per SIMD (registers capped at 256): one wave's softmax overlaps the
 // other's matrix products
 template <int D, int NW>
-__global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a) {
+__global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a0) {
+  const AttnArgs a = attn_seq_view<uint16_t>(a0);
   using T = Tile<D>;
   constexpr int NTH = 64 * NW, BKV = 64, KS = D / 16, JB = D / 32, ST = 2;
   constexpr int TILE = BKV * D, STAGE = 2 * TILE;       // elements: K then V
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   const int h = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int G = lane >> 5, c = lane & 31, H = a.H;
+  const int G = lane >> 5, c = lane & 31, H = a.ld;  // H: row stride
   const int q_lo = a.l + blockIdx.x * 32 * NW;       // first query of the block
   const int t = q_lo + 32 * w + c;                    // this lane's query
   const bool tvalid = t < a.r;
@@ -316,13 +317,14 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a) {
 
 // D[h][t] = sum_j dO[t][h d + j] * O[t][h d + j]; one wave per (row, head).
 template <int D>
-__global__ __launch_bounds__(256) void attn_bwd_rowdot(AttnArgs a) {
+__global__ __launch_bounds__(256) void attn_bwd_rowdot(AttnArgs a0) {
+  const AttnArgs a = attn_seq_view<uint16_t>(a0);
   const int wave = (blockIdx.x * 256 + threadIdx.x) >> 6, lane = threadIdx.x & 63;
   const int n = a.r - a.l;
   if (wave >= n * a.heads) return;
   const int i = wave / a.heads, h = wave % a.heads;
-  const uint16_t* dO = (const uint16_t*)a.dout + (long)i * a.H + h * D;
-  const uint16_t* O = (const uint16_t*)a.o + (long)i * a.H + h * D;
+  const uint16_t* dO = (const uint16_t*)a.dout + (long)i * a.ld + h * D;
+  const uint16_t* O = (const uint16_t*)a.o + (long)i * a.ld + h * D;
   float s = 0.f;
   for (int j = lane; j < D; j += 64) s += to_f32(bf16{dO[j]}) * to_f32(bf16{O[j]});
   s = wave_sum(s);
@@ -337,7 +339,8 @@ __global__ __launch_bounds__(256) void attn_bwd_rowdot(AttnArgs a) {
 // ST query tiles form the LDS ring: tile qb + ST - 1 is requested while tile
 // qb is multiplied.
 template <int D, int NW, int MODE, int ST>
-__global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma(AttnArgs a) {
+__global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma(AttnArgs a0) {
+  const AttnArgs a = attn_seq_view<uint16_t>(a0);
   using T = Tile<D>;
   constexpr bool DO_K = MODE != 1, DO_V = MODE != 2;
   constexpr int NTH = 64 * NW, BQ = 32, KS = D / 16, JB = D / 32;
@@ -346,7 +349,7 @@ __global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma
   constexpr int PER_ISSUE = 2 * (BQ * D / 8) / NTH + 1;  // DMA instructions per tile
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   const int h = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int G = lane >> 5, c = lane & 31, H = a.H;
+  const int G = lane >> 5, c = lane & 31, H = a.ld;  // H: row stride
   const int k_lo = blockIdx.x * 32 * NW;     // first key of the block
   const int s_w = k_lo + 32 * w;             // first key of this wave
   const int s_me = s_w + c;                  // this lane's key (column of S)
@@ -571,13 +574,14 @@ __global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma
 // ------------------------------------------------------------------- dQ
 
 template <int D, int NW>
-__global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a) {
+__global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a0) {
+  const AttnArgs a = attn_seq_view<uint16_t>(a0);
   using T = Tile<D>;
   constexpr int NTH = 64 * NW, BKV = 64, KS = D / 16, JB = D / 32, ST = 2;
   constexpr int TILE = BKV * D, STAGE = 2 * TILE;  // K then V
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   const int h = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int G = lane >> 5, c = lane & 31, H = a.H;
+  const int G = lane >> 5, c = lane & 31, H = a.ld;  // H: row stride
   const int q_lo = a.l + blockIdx.x * 32 * NW;
   const int t = q_lo + 32 * w + c;
   const bool tvalid = t < a.r;
@@ -709,14 +713,14 @@ hipError_t fwd_d(const AttnArgs& a, hipStream_t s) {
   constexpr size_t lds = 2 * 2 * 64 * D * 2;
   hipError_t e = set_lds(attn_fwd_mfma<D, NWF>, lds);
   if (e != hipSuccess) return e;
-  attn_fwd_mfma<D, NWF><<<dim3(cdiv(n, 32 * NWF), a.heads), 64 * NWF, lds, s>>>(a);
+  attn_fwd_mfma<D, NWF><<<dim3(cdiv(n, 32 * NWF), a.heads, a.bs), 64 * NWF, lds, s>>>(a);
   return hipGetLastError();
 }
 
 template <int D>
 hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
   const int n = a.r - a.l;
-  attn_bwd_rowdot<D><<<cdiv((long)n * a.heads, 4), 256, 0, s>>>(a);
+  attn_bwd_rowdot<D><<<dim3(cdiv((long)n * a.heads, 4), 1, a.bs), 256, 0, s>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // dV kernel: 4 waves, a 4-tile ring (69 KB, two blocks per CU).  dK kernel:
@@ -730,28 +734,29 @@ hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
   e = set_lds(attn_bwd_dkdv_mfma<D, NWF, DKDV_MODE_A, STA>, lds_a);
   if (e != hipSuccess) return e;
   attn_bwd_dkdv_mfma<D, NWF, DKDV_MODE_A, STA>
-      <<<dim3(cdiv(a.r, 32 * NWF), a.heads), 64 * NWF, lds_a, s>>>(a);
+      <<<dim3(cdiv(a.r, 32 * NWF), a.heads, a.bs), 64 * NWF, lds_a, s>>>(a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if constexpr (DKDV_MODE_A != 0) {
     e = set_lds(attn_bwd_dkdv_mfma<D, NWK, 2, STK>, lds_k);
     if (e != hipSuccess) return e;
     attn_bwd_dkdv_mfma<D, NWK, 2, STK>
-        <<<dim3(cdiv(a.r, 32 * NWK), a.heads), 64 * NWK, lds_k, s>>>(a);
+        <<<dim3(cdiv(a.r, 32 * NWK), a.heads, a.bs), 64 * NWK, lds_k, s>>>(a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   constexpr size_t lds_q = 2 * 2 * 64 * D * 2;
   e = set_lds(attn_bwd_dq_mfma<D, NWF>, lds_q);
   if (e != hipSuccess) return e;
-  attn_bwd_dq_mfma<D, NWF><<<dim3(cdiv(n, 32 * NWF), a.heads), 64 * NWF, lds_q, s>>>(a);
+  attn_bwd_dq_mfma<D, NWF><<<dim3(cdiv(n, 32 * NWF), a.heads, a.bs), 64 * NWF, lds_q, s>>>(a);
   return hipGetLastError();
 }
 
 inline bool al16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 bool covered(const AttnArgs& a) {
-  return (a.d == 64 || a.d == 128) && (a.H % 8) == 0 && al16(a.q) && al16(a.kc) && al16(a.vc);
+  return (a.d == 64 || a.d == 128) && (a.H % 8) == 0 && (a.ld % 8) == 0 && al16(a.q) &&
+         al16(a.kc) && al16(a.vc);
 }
 
 }  // namespace
@@ -762,7 +767,8 @@ hipError_t attn_fwd_mfma_bf16(const AttnArgs& a, hipStream_t s) {
 }
 
 hipError_t attn_bwd_mfma_bf16(const AttnArgs& a, hipStream_t s) {
-  if (!covered(a) || !al16(a.dout) || !al16(a.dq) || (a.ld_dq % 8)) return hipErrorNotSupported;
+  if (!covered(a) || !al16(a.dout) || !al16(a.dq) || (a.ld_dq % 8) || (a.dq_seq % 8))
+    return hipErrorNotSupported;
   return a.d == 128 ? bwd_d<128>(a, s) : bwd_d<64>(a, s);
 }
 

@@ -125,9 +125,10 @@ hipError_t gemm_generic(int dtype, const GemmArgs& a, hipStream_t s) {
 // One block per (query row, head).  LDS: scores [Lmax] (+ dP [Lmax] for bwd),
 // q and dO rows, reduction scratch.
 template <typename T>
-__global__ __launch_bounds__(256) void attn_fwd_generic_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256) void attn_fwd_generic_kernel(AttnArgs a0) {
   extern __shared__ float sm[];
-  const int i = blockIdx.x, t = a.l + i, h = blockIdx.y, d = a.d, H = a.H;
+  const AttnArgs a = attn_seq_view<T>(a0);
+  const int i = blockIdx.x, t = a.l + i, h = blockIdx.y, d = a.d, H = a.ld;  // H: row stride
   float* S = sm;
   float* qs = sm + a.Lmax;
   float* red = qs + 128;
@@ -161,9 +162,10 @@ __global__ __launch_bounds__(256) void attn_fwd_generic_kernel(AttnArgs a) {
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void attn_bwd_generic_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256) void attn_bwd_generic_kernel(AttnArgs a0) {
   extern __shared__ float sm[];
-  const int i = blockIdx.x, t = a.l + i, h = blockIdx.y, d = a.d, H = a.H;
+  const AttnArgs a = attn_seq_view<T>(a0);
+  const int i = blockIdx.x, t = a.l + i, h = blockIdx.y, d = a.d, H = a.ld;  // H: row stride
   float* P = sm;
   float* dS = sm + a.Lmax;
   float* qs = dS + a.Lmax;
@@ -215,7 +217,7 @@ static hipError_t attn_generic_t(const AttnArgs& a, bool bwd, hipStream_t s) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  dim3 grid(a.r - a.l, a.heads);
+  dim3 grid(a.r - a.l, a.heads, a.bs);
   if (bwd)
     attn_bwd_generic_kernel<T><<<grid, 256, lds, s>>>(a);
   else

@@ -148,3 +148,68 @@ extern "C" tp_status tp_dp_optimal_slicing(const int64_t* cost, int L_units, int
   *out_T = sum + (int64_t)(K - 1) * mx;
   return TP_OK;
 }
+
+// Batch splitting (Sec. 3.4, combining token slicing with batch slicing): a
+// batch of B sequences is cut into groups of b_1 + ... + b_D = B sequences
+// that go through the pipeline one group after another, each with its own
+// optimal token slicing; the group sizes minimise T_{b_1} + ... + T_{b_D}, a
+// one-dimensional knapsack over the per-size latencies T_b.
+//
+// best[x] = the smallest total over groups that sum to x sequences:
+// best[0] = 0, best[x] = min over b = 1..x (T_b >= 0) of best[x - b] + T_b,
+// b scanned ascending and replaced only on a strictly smaller total (the last
+// group is the smallest one that attains the minimum).  The groups are then
+// reported largest first.
+tp_status tp_dp_batch_split(const int64_t* T_b, int B, int* out_sizes, int* out_D,
+                            int64_t* out_total) {
+  if (!T_b || !out_sizes || !out_D || !out_total || B < 1) return TP_ERR_INVALID;
+  std::vector<int64_t> best(B + 1, INF);
+  std::vector<int> last(B + 1, 0);
+  best[0] = 0;
+  for (int x = 1; x <= B; ++x)
+    for (int b = 1; b <= x; ++b) {
+      const int64_t t = T_b[b - 1];
+      if (t < 0 || best[x - b] == INF) continue;
+      if (best[x - b] > INF - t) return TP_ERR_INVALID;  // overflow
+      const int64_t v = best[x - b] + t;
+      if (v < best[x]) {
+        best[x] = v;
+        last[x] = b;
+      }
+    }
+  if (best[B] == INF) return TP_ERR_INVALID;
+  std::vector<int> sizes;
+  for (int x = B; x > 0; x -= last[x]) sizes.push_back(last[x]);
+  std::sort(sizes.begin(), sizes.end(), [](int a, int b) { return a > b; });
+  for (size_t i = 0; i < sizes.size(); ++i) out_sizes[i] = sizes[i];
+  *out_D = (int)sizes.size();
+  *out_total = best[B];
+  return TP_OK;
+}
+
+// Joint batch x token plan (Sec. 3.4): the token DP of Sec. 3.3 for every
+// group size b = 1..B on that size's cost table, then the batch split over the
+// resulting T_b.
+tp_status tp_dp_joint_slicing(const int64_t* costs, int B, int L_units, int unit, int K,
+                              int64_t eps_ns, int* out_sizes, int* out_D, int* out_lens,
+                              int* out_M, int64_t* out_T_b, int64_t* out_total) {
+  if (!costs || !out_sizes || !out_D || !out_lens || !out_M || !out_T_b || !out_total || B < 1 ||
+      L_units < 1)
+    return TP_ERR_INVALID;
+  const size_t plane = (size_t)L_units * L_units;
+  std::vector<std::vector<int>> lens(B, std::vector<int>(L_units));
+  std::vector<int> M(B, 0);
+  for (int b = 1; b <= B; ++b) {
+    const tp_status s = tp_dp_optimal_slicing(costs + (b - 1) * plane, L_units, unit, K, eps_ns,
+                                              lens[b - 1].data(), &M[b - 1], &out_T_b[b - 1]);
+    if (s != TP_OK) return s;
+  }
+  const tp_status s = tp_dp_batch_split(out_T_b, B, out_sizes, out_D, out_total);
+  if (s != TP_OK) return s;
+  for (int g = 0; g < *out_D; ++g) {
+    const int b = out_sizes[g];
+    out_M[g] = M[b - 1];
+    std::copy(lens[b - 1].begin(), lens[b - 1].begin() + M[b - 1], out_lens + (size_t)g * L_units);
+  }
+  return TP_OK;
+}

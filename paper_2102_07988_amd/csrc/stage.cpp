@@ -63,6 +63,7 @@ struct PendingTiming {
 struct tp_stage {
   tp_stage_config cfg;
   int H, F, heads, d, L, dt;
+  int bsz;  // sequences per batch slice: token t of sequence s is row t * bsz + s
   size_t esz;
   std::vector<tp_layer_ptrs> P, G;
   std::vector<LayerBufs> lb;
@@ -88,8 +89,11 @@ bool config_ok(const tp_stage_config* c) {
   if (c->dtype != TP_DTYPE_BF16 && c->dtype != TP_DTYPE_FP32) return false;
   if (c->wgrad_mode != TP_WGRAD_PER_SLICE && c->wgrad_mode != TP_WGRAD_DEFERRED) return false;
   if (!(c->ln_eps > 0.f) || !std::isfinite(c->ln_eps)) return false;
+  if (c->batch < 0 || c->batch > 64) return false;
   return true;
 }
+
+int batch_of(const tp_stage_config* c) { return c->batch > 0 ? c->batch : 1; }
 
 bool config_supported(const tp_stage_config* c) {
   const int d = c->hidden / c->heads;
@@ -103,7 +107,8 @@ bool config_supported(const tp_stage_config* c) {
 size_t carve(const tp_stage_config* c, void* base, std::vector<LayerBufs>* lbs, Scratch* sc) {
   Carver cv(base);
   const size_t esz = c->dtype == TP_DTYPE_FP32 ? 4 : 2;
-  const size_t L = c->max_seq, H = c->hidden, F = 4 * H, a = c->heads;
+  // every per-token arena holds max_seq * batch rows
+  const size_t L = (size_t)c->max_seq * batch_of(c), H = c->hidden, F = 4 * H, a = c->heads;
   for (int i = 0; i < c->n_layers; ++i) {
     LayerBufs b;
     b.x_in = cv.take(L * H * esz);
@@ -222,6 +227,7 @@ GemmArgs tn(int M, int N, int K, const void* dY, long ldy, const void* X, long l
   return g;
 }
 
+// rows [l, l + n) of the per-token arenas
 tp_status wgrad_gemms(tp_stage* S, int li, int l, int n) {
   const int H = S->H, F = S->F;
   const size_t e = S->esz;
@@ -239,51 +245,56 @@ tp_status wgrad_gemms(tp_stage* S, int li, int l, int n) {
 }
 
 tp_status forward_impl(tp_stage* S, int l, int r, const void* x, void* y) {
-  const int H = S->H, F = S->F, n = r - l, NL = S->cfg.n_layers, dt = S->dt;
+  const int H = S->H, F = S->F, NL = S->cfg.n_layers, dt = S->dt;
+  // batch slice: tokens [l, r) of bsz sequences are rows [lr, lr + n)
+  const int ntok = r - l, lr = l * S->bsz, n = ntok * S->bsz;
   const size_t e = S->esz;
   hipStream_t st = S->stream;
   const double nb = (double)n * H * e;
   for (int li = 0; li < NL; ++li) {
     LayerBufs& B = S->lb[li];
     const tp_layer_ptrs& P = S->P[li];
-    void* xin = rowp(B.x_in, l, H, e);
+    void* xin = rowp(B.x_in, lr, H, e);
     TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
       return ln_fwd(dt, n, H, li == 0 ? x : xin, li == 0 ? xin : nullptr, P.ln1_g, P.ln1_b,
-                    rowp(B.u, l, H, e), B.mean1 + l, B.rstd1 + l, S->cfg.ln_eps, st);
+                    rowp(B.u, lr, H, e), B.mean1 + lr, B.rstd1 + lr, S->cfg.ln_eps, st);
     }));
-    GemmArgs g = nt(n, 3 * H, H, rowp(B.u, l, H, e), H, P.w_qkv);
+    GemmArgs g = nt(n, 3 * H, H, rowp(B.u, lr, H, e), H, P.w_qkv);
     g.epi = EPI_QKV;
     g.bias = P.b_qkv;
-    g.q = rowp(B.q, l, H, e), g.k = rowp(B.kc, l, H, e), g.v = rowp(B.vc, l, H, e), g.H = H;
+    g.q = rowp(B.q, lr, H, e), g.k = rowp(B.kc, lr, H, e), g.v = rowp(B.vc, lr, H, e), g.H = H;
     TRY(run_gemm(S, K_GEMM_FWD, g));
     AttnArgs a;
     a.l = l, a.r = r, a.H = H, a.heads = S->heads, a.d = S->d, a.Lmax = S->L;
+    a.bs = S->bsz, a.ld = S->bsz * H;
     a.scale = 1.f / std::sqrt((float)S->d);
-    a.q = rowp(B.q, l, H, e), a.kc = B.kc, a.vc = B.vc, a.o = rowp(B.o, l, H, e), a.lse = B.lse;
-    const double pairs = (double)n * l + (double)n * (n + 1) / 2;
-    TRY(launch(S, K_ATTN_FWD, 4.0 * H * pairs, (2.0 * n + 2.0 * r) * H * e,
+    a.q = rowp(B.q, lr, H, e), a.kc = B.kc, a.vc = B.vc, a.o = rowp(B.o, lr, H, e), a.lse = B.lse;
+    const double pairs = ((double)ntok * l + (double)ntok * (ntok + 1) / 2) * S->bsz;
+    TRY(launch(S, K_ATTN_FWD, 4.0 * H * pairs, (2.0 * ntok + 2.0 * r) * S->bsz * H * e,
                [&] { return attn_fwd(dt, a, st); }));
-    g = nt(n, H, H, rowp(B.o, l, H, e), H, P.w_o);
-    g.epi = EPI_RESID, g.bias = P.b_o, g.R = xin, g.ldr = H, g.C = rowp(B.x1, l, H, e), g.ldc = H;
+    g = nt(n, H, H, rowp(B.o, lr, H, e), H, P.w_o);
+    g.epi = EPI_RESID, g.bias = P.b_o, g.R = xin, g.ldr = H, g.C = rowp(B.x1, lr, H, e), g.ldc = H;
     TRY(run_gemm(S, K_GEMM_FWD, g));
     TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
-      return ln_fwd(dt, n, H, rowp(B.x1, l, H, e), nullptr, P.ln2_g, P.ln2_b,
-                    rowp(B.u2, l, H, e), B.mean2 + l, B.rstd2 + l, S->cfg.ln_eps, st);
+      return ln_fwd(dt, n, H, rowp(B.x1, lr, H, e), nullptr, P.ln2_g, P.ln2_b,
+                    rowp(B.u2, lr, H, e), B.mean2 + lr, B.rstd2 + lr, S->cfg.ln_eps, st);
     }));
-    g = nt(n, F, H, rowp(B.u2, l, H, e), H, P.w_fc1);
-    g.epi = EPI_GELU, g.bias = P.b_fc1, g.C = rowp(B.z, l, F, e), g.ldc = F;
-    g.C2 = rowp(B.g, l, F, e), g.ldc2 = F;
+    g = nt(n, F, H, rowp(B.u2, lr, H, e), H, P.w_fc1);
+    g.epi = EPI_GELU, g.bias = P.b_fc1, g.C = rowp(B.z, lr, F, e), g.ldc = F;
+    g.C2 = rowp(B.g, lr, F, e), g.ldc2 = F;
     TRY(run_gemm(S, K_GEMM_FWD, g));
-    g = nt(n, H, F, rowp(B.g, l, F, e), F, P.w_fc2);
-    g.epi = EPI_RESID, g.bias = P.b_fc2, g.R = rowp(B.x1, l, H, e), g.ldr = H;
-    g.C = li == NL - 1 ? y : rowp(S->lb[li + 1].x_in, l, H, e), g.ldc = H;
+    g = nt(n, H, F, rowp(B.g, lr, F, e), F, P.w_fc2);
+    g.epi = EPI_RESID, g.bias = P.b_fc2, g.R = rowp(B.x1, lr, H, e), g.ldr = H;
+    g.C = li == NL - 1 ? y : rowp(S->lb[li + 1].x_in, lr, H, e), g.ldc = H;
     TRY(run_gemm(S, K_GEMM_FWD, g));
   }
   return TP_OK;
 }
 
 tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
-  const int H = S->H, F = S->F, n = r - l, NL = S->cfg.n_layers, dt = S->dt;
+  const int H = S->H, F = S->F, NL = S->cfg.n_layers, dt = S->dt;
+  // batch slice: tokens [l, r) of bsz sequences are rows [lr, lr + n)
+  const int ntok = r - l, lr = l * S->bsz, n = ntok * S->bsz;
   const size_t e = S->esz;
   hipStream_t st = S->stream;
   const bool per_slice = S->cfg.wgrad_mode == TP_WGRAD_PER_SLICE;
@@ -292,77 +303,79 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
     LayerBufs& B = S->lb[li];
     const tp_layer_ptrs& P = S->P[li];
     tp_layer_ptrs& G = S->G[li];
-    void* dyl = rowp(B.dy, l, H, e);
+    void* dyl = rowp(B.dy, lr, H, e);
     if (li == NL - 1)
       TRY(launch(S, K_MISC, 0, 2 * nb, [&] { return copy_rows(dt, n, H, dy, dyl, st); }));
     // FC2 backward (dX fused with GELU'): dz = (dy W2) * GELU'(z)
     GemmArgs g = nn(n, F, H, dyl, H, P.w_fc2);
-    g.epi = EPI_DGELU, g.R = rowp(B.z, l, F, e), g.ldr = F, g.C = rowp(B.dz, l, F, e), g.ldc = F;
+    g.epi = EPI_DGELU, g.R = rowp(B.z, lr, F, e), g.ldr = F, g.C = rowp(B.dz, lr, F, e), g.ldc = F;
     TRY(run_gemm(S, K_GEMM_DX, g));
     TRY(launch(S, K_MISC, 0, nb, [&] { return colsum_acc(dt, n, H, dyl, H, (float*)G.b_fc2, st); }));
     // FC1 backward: du2 = dz W1
-    g = nn(n, H, F, rowp(B.dz, l, F, e), F, P.w_fc1);
+    g = nn(n, H, F, rowp(B.dz, lr, F, e), F, P.w_fc1);
     g.C = S->sc.du2, g.ldc = H;
     TRY(run_gemm(S, K_GEMM_DX, g));
     TRY(launch(S, K_MISC, 0, (double)n * F * e, [&] {
-      return colsum_acc(dt, n, F, rowp(B.dz, l, F, e), F, (float*)G.b_fc1, st);
+      return colsum_acc(dt, n, F, rowp(B.dz, lr, F, e), F, (float*)G.b_fc1, st);
     }));
     // LN2 backward + residual: dx1 = dy + LN2^T(du2)
     TRY(launch(S, K_NORM, 0, 4 * nb, [&] {
-      return ln_bwd(dt, n, H, S->sc.du2, rowp(B.x1, l, H, e), B.mean2 + l, B.rstd2 + l, P.ln2_g,
-                    dyl, rowp(B.dx1, l, H, e), st);
+      return ln_bwd(dt, n, H, S->sc.du2, rowp(B.x1, lr, H, e), B.mean2 + lr, B.rstd2 + lr, P.ln2_g,
+                    dyl, rowp(B.dx1, lr, H, e), st);
     }));
     TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
-      return ln_param_grads(dt, n, H, S->sc.du2, rowp(B.x1, l, H, e), B.mean2 + l, B.rstd2 + l,
+      return ln_param_grads(dt, n, H, S->sc.du2, rowp(B.x1, lr, H, e), B.mean2 + lr, B.rstd2 + lr,
                             (float*)G.ln2_g, (float*)G.ln2_b, st);
     }));
     // output projection backward: dO = dx1 W_o
-    g = nn(n, H, H, rowp(B.dx1, l, H, e), H, P.w_o);
+    g = nn(n, H, H, rowp(B.dx1, lr, H, e), H, P.w_o);
     g.C = S->sc.dout, g.ldc = H;
     TRY(run_gemm(S, K_GEMM_DX, g));
     TRY(launch(S, K_MISC, 0, nb, [&] {
-      return colsum_acc(dt, n, H, rowp(B.dx1, l, H, e), H, (float*)G.b_o, st);
+      return colsum_acc(dt, n, H, rowp(B.dx1, lr, H, e), H, (float*)G.b_o, st);
     }));
     // attention backward: dq rows, dK/dV into the fp32 buffer for keys [0, r)
     AttnArgs a;
     a.l = l, a.r = r, a.H = H, a.heads = S->heads, a.d = S->d, a.Lmax = S->L;
+    a.bs = S->bsz, a.ld = S->bsz * H;
     a.scale = 1.f / std::sqrt((float)S->d);
-    a.q = rowp(B.q, l, H, e), a.kc = B.kc, a.vc = B.vc, a.o = rowp(B.o, l, H, e), a.lse = B.lse;
+    a.q = rowp(B.q, lr, H, e), a.kc = B.kc, a.vc = B.vc, a.o = rowp(B.o, lr, H, e), a.lse = B.lse;
     a.dout = S->sc.dout, a.D = S->sc.D;
-    a.dq = rowp(B.dqkv, l, 3 * H, e), a.ld_dq = 3 * H;
+    a.dq = rowp(B.dqkv, lr, 3 * H, e), a.ld_dq = (long)S->bsz * 3 * H, a.dq_seq = 3 * H;
     a.dk = B.dk, a.dv = B.dv;
-    const double pairs = (double)n * l + (double)n * (n + 1) / 2;
-    TRY(launch(S, K_ATTN_BWD, 8.0 * H * pairs, (4.0 * n + 2.0 * r) * H * e + 16.0 * r * H,
+    const double pairs = ((double)ntok * l + (double)ntok * (ntok + 1) / 2) * S->bsz;
+    TRY(launch(S, K_ATTN_BWD, 8.0 * H * pairs,
+               ((4.0 * ntok + 2.0 * r) * H * e + 16.0 * r * H) * S->bsz,
                [&] { return attn_bwd(dt, a, st); }));
     TRY(launch(S, K_MISC, 0, 8.0 * n * H + 2 * nb, [&] {
-      return pack_dkv(dt, n, H, B.dk + (long)l * H, B.dv + (long)l * H,
-                      rowp(B.dqkv, l, 3 * H, e), st);
+      return pack_dkv(dt, n, H, B.dk + (long)lr * H, B.dv + (long)lr * H,
+                      rowp(B.dqkv, lr, 3 * H, e), st);
     }));
     // QKV backward: du = [dq dk dv] W_qkv
-    g = nn(n, H, 3 * H, rowp(B.dqkv, l, 3 * H, e), 3 * H, P.w_qkv);
+    g = nn(n, H, 3 * H, rowp(B.dqkv, lr, 3 * H, e), 3 * H, P.w_qkv);
     g.C = S->sc.du, g.ldc = H;
     TRY(run_gemm(S, K_GEMM_DX, g));
     TRY(launch(S, K_MISC, 0, 3 * nb, [&] {
-      return colsum_acc(dt, n, 3 * H, rowp(B.dqkv, l, 3 * H, e), 3 * H, (float*)G.b_qkv, st);
+      return colsum_acc(dt, n, 3 * H, rowp(B.dqkv, lr, 3 * H, e), 3 * H, (float*)G.b_qkv, st);
     }));
     // LN1 backward + residual: dx = dx1 + LN1^T(du)
-    void* out = li == 0 ? dx : rowp(S->lb[li - 1].dy, l, H, e);
+    void* out = li == 0 ? dx : rowp(S->lb[li - 1].dy, lr, H, e);
     TRY(launch(S, K_NORM, 0, 4 * nb, [&] {
-      return ln_bwd(dt, n, H, S->sc.du, rowp(B.x_in, l, H, e), B.mean1 + l, B.rstd1 + l, P.ln1_g,
-                    rowp(B.dx1, l, H, e), out, st);
+      return ln_bwd(dt, n, H, S->sc.du, rowp(B.x_in, lr, H, e), B.mean1 + lr, B.rstd1 + lr, P.ln1_g,
+                    rowp(B.dx1, lr, H, e), out, st);
     }));
     TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
-      return ln_param_grads(dt, n, H, S->sc.du, rowp(B.x_in, l, H, e), B.mean1 + l, B.rstd1 + l,
+      return ln_param_grads(dt, n, H, S->sc.du, rowp(B.x_in, lr, H, e), B.mean1 + lr, B.rstd1 + lr,
                             (float*)G.ln1_g, (float*)G.ln1_b, st);
     }));
     if (per_slice) {
-      tp_status s = wgrad_gemms(S, li, l, n);
+      tp_status s = wgrad_gemms(S, li, lr, n);
       if (s != TP_OK) return s;
     }
   }
   if (!per_slice && l == 0 && !S->profiling) {
     for (int li = NL - 1; li >= 0; --li) {
-      tp_status s = wgrad_gemms(S, li, 0, S->cached_len);
+      tp_status s = wgrad_gemms(S, li, 0, S->cached_len * S->bsz);
       if (s != TP_OK) return s;
     }
   }
@@ -405,6 +418,7 @@ tp_status tp_stage_init(const tp_stage_config* cfg, const tp_layer_ptrs* params,
   S->heads = cfg->heads;
   S->d = cfg->hidden / cfg->heads;
   S->L = cfg->max_seq;
+  S->bsz = batch_of(cfg);
   S->dt = cfg->dtype == TP_DTYPE_FP32 ? DT_FP32 : DT_BF16;
   S->esz = cfg->dtype == TP_DTYPE_FP32 ? 4 : 2;
   S->P.assign(params, params + cfg->n_layers);
@@ -427,7 +441,7 @@ void tp_stage_destroy(tp_stage* S) {
 
 tp_status tp_kv_prefix_reset(tp_stage* S) {
   if (!S) return TP_ERR_INVALID;
-  const size_t n = (size_t)S->L * S->H;
+  const size_t n = (size_t)S->L * S->bsz * S->H;
   for (auto& B : S->lb) {
     TRY(fill_f32(B.dk, n, 0.f, S->stream));
     TRY(fill_f32(B.dv, n, 0.f, S->stream));
@@ -479,7 +493,7 @@ tp_status tp_profile_slice_cost(tp_stage* S, const int* lens, int n_lens, const 
   S->profiling = true;
   tp_status status = TP_OK;
   // deterministic, finite slice inputs
-  const size_t io = (size_t)S->L * S->H;
+  const size_t io = (size_t)S->L * S->bsz * S->H;
   if (S->dt == DT_FP32) {
     if (fill_f32((float*)S->sc.io_a, io, 0.5f, S->stream) != hipSuccess) status = TP_ERR_HIP;
   } else {

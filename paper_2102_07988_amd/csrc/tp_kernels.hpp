@@ -56,8 +56,15 @@ hipError_t gemm_generic(int dtype, const GemmArgs& a, hipStream_t s);
 // Prefix-causal attention over a slice: queries t in [l, r), keys s in [0, t].
 // q, o: rows [r-l][H] (row i = token l+i); kc, vc: cache rows [Lmax][H] from
 // token 0; lse: fp32 [heads][Lmax] (absolute token index).
+// A batch of bs sequences shares the token positions: row t * bs + s holds
+// token t of sequence s (bs = 1: row t).  Every row-indexed tensor below
+// (q, o, dout: the slice's rows; kc, vc, dk, dv: absolute rows) has row stride
+// ld = bs * H elements and sequence s starts at column s * H; dq has row stride
+// ld_dq and sequence s at column s * dq_seq; lse and D hold one [heads][Lmax]
+// plane per sequence.  Kernels take the sequence from blockIdx.z.
 struct AttnArgs {
   int l = 0, r = 0, H = 0, heads = 0, d = 0, Lmax = 0;
+  int bs = 1, ld = 0;
   float scale = 1.f;
   const void* q = nullptr;
   const void* kc = nullptr;
@@ -65,13 +72,33 @@ struct AttnArgs {
   void* o = nullptr;
   float* lse = nullptr;
   // backward
-  const void* dout = nullptr;  // [r-l][H]
-  float* D = nullptr;          // fp32 [heads][Lmax] scratch: rowsum(dO * O)
-  void* dq = nullptr;          // rows of ld_dq elements (row i = token l+i)
-  long ld_dq = 0;
-  float* dk = nullptr;  // fp32 [Lmax][H] accumulation buffers (absolute rows)
+  const void* dout = nullptr;  // the slice's rows
+  float* D = nullptr;          // fp32 [bs][heads][Lmax] scratch: rowsum(dO * O)
+  void* dq = nullptr;          // the slice's rows, ld_dq elements apart
+  long ld_dq = 0, dq_seq = 0;
+  float* dk = nullptr;  // fp32 accumulation buffers (absolute rows)
   float* dv = nullptr;
 };
+// The arguments of sequence blockIdx.z of the batch as a one-sequence view:
+// pointers moved to its columns (element type T) and planes; the row stride
+// stays a.ld.
+template <typename T>
+__device__ inline AttnArgs attn_seq_view(AttnArgs a) {
+  const int s = blockIdx.z;
+  if (s == 0) return a;
+  const long off = (long)s * a.H, plane = (long)s * a.heads * a.Lmax;
+  a.q = (const T*)a.q + off;
+  a.kc = (const T*)a.kc + off;
+  a.vc = (const T*)a.vc + off;
+  if (a.o) a.o = (T*)a.o + off;
+  if (a.dout) a.dout = (const T*)a.dout + off;
+  if (a.dq) a.dq = (T*)a.dq + s * a.dq_seq;
+  if (a.dk) a.dk += off;
+  if (a.dv) a.dv += off;
+  if (a.lse) a.lse += plane;
+  if (a.D) a.D += plane;
+  return a;
+}
 hipError_t attn_fwd(int dtype, const AttnArgs& a, hipStream_t s);
 hipError_t attn_bwd(int dtype, const AttnArgs& a, hipStream_t s);
 

@@ -81,6 +81,20 @@ def upstream_grad(seq: int, hidden: int, seed: int = SEED_DY, dtype=torch.float3
     return normal((seq, hidden), seed, 2, 1.0, 0.0, dtype, device)
 
 
+def batch_hidden_states(seq: int, batch: int, hidden: int, seed: int = SEED_X,
+                        dtype=torch.float32, device="cpu") -> torch.Tensor:
+    """[seq, batch, hidden]: sequence s is hidden_states(seq, hidden, seed * 1000 + s)."""
+    return torch.stack([hidden_states(seq, hidden, seed * 1000 + s, dtype, device)
+                        for s in range(batch)], dim=1)
+
+
+def batch_upstream_grad(seq: int, batch: int, hidden: int, seed: int = SEED_DY,
+                        dtype=torch.float32, device="cpu") -> torch.Tensor:
+    """[seq, batch, hidden]: sequence s is upstream_grad(seq, hidden, seed * 1000 + s)."""
+    return torch.stack([upstream_grad(seq, hidden, seed * 1000 + s, dtype, device)
+                        for s in range(batch)], dim=1)
+
+
 def to_f64(t: torch.Tensor) -> np.ndarray:
     return t.detach().to("cpu", torch.float64).numpy().copy()
 

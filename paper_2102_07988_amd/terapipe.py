@@ -29,7 +29,8 @@ SYNTH_NAMES = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
 
 EXPORTED = ("tp_stage_workspace_bytes", "tp_stage_init", "tp_stage_destroy",
             "tp_kv_prefix_reset", "tp_slice_forward", "tp_slice_backward",
-            "tp_profile_slice_cost", "tp_dp_optimal_slicing", "tp_fit_ctx_model",
+            "tp_profile_slice_cost", "tp_dp_optimal_slicing", "tp_dp_batch_split",
+            "tp_dp_joint_slicing", "tp_fit_ctx_model",
             "tp_cost_table_from_model", "tp_profile_cost_model", "tp_status_string",
             "tp_stage_enable_kernel_timing", "tp_stage_kernel_stats", "tp_measure_mfma_peak")
 
@@ -37,7 +38,7 @@ EXPORTED = ("tp_stage_workspace_bytes", "tp_stage_init", "tp_stage_destroy",
 class StageConfig(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int), ("hidden", ctypes.c_int), ("heads", ctypes.c_int),
                 ("max_seq", ctypes.c_int), ("dtype", ctypes.c_int), ("wgrad_mode", ctypes.c_int),
-                ("ln_eps", ctypes.c_float)]
+                ("ln_eps", ctypes.c_float), ("batch", ctypes.c_int)]
 
 
 class LayerPtrs(ctypes.Structure):
@@ -81,6 +82,11 @@ def _load():
     lib.tp_dp_optimal_slicing.restype = ctypes.c_int
     lib.tp_dp_optimal_slicing.argtypes = [i64p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                           ctypes.c_int64, ip, ip, i64p]
+    lib.tp_dp_batch_split.restype = ctypes.c_int
+    lib.tp_dp_batch_split.argtypes = [i64p, ctypes.c_int, ip, ip, i64p]
+    lib.tp_dp_joint_slicing.restype = ctypes.c_int
+    lib.tp_dp_joint_slicing.argtypes = [i64p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                        ctypes.c_int, ctypes.c_int64, ip, ip, ip, ip, i64p, i64p]
     dp = ctypes.POINTER(ctypes.c_double)
     lib.tp_fit_ctx_model.restype = ctypes.c_int
     lib.tp_fit_ctx_model.argtypes = [i64p, ctypes.c_int, ctypes.c_int, ip, ip, i64p, ctypes.c_int,
@@ -114,10 +120,10 @@ def _check(status: int, what: str):
 
 
 def make_config(n_layers: int, hidden: int, heads: int, max_seq: int, dtype: str = "bf16",
-                wgrad: str = "per_slice", ln_eps: float = 1e-5) -> StageConfig:
+                wgrad: str = "per_slice", ln_eps: float = 1e-5, batch: int = 1) -> StageConfig:
     return StageConfig(n_layers, hidden, heads, max_seq,
                        DTYPE_BF16 if dtype == "bf16" else DTYPE_FP32,
-                       WGRAD_PER_SLICE if wgrad == "per_slice" else WGRAD_DEFERRED, ln_eps)
+                       WGRAD_PER_SLICE if wgrad == "per_slice" else WGRAD_DEFERRED, ln_eps, batch)
 
 
 def workspace_bytes(cfg: StageConfig) -> int:
@@ -139,17 +145,19 @@ class Stage:
     (ln1_g, ..., w1, b1, w2, b2), device tensors of the stage dtype, weights
     [out, in].  Gradients are fp32 device tensors in ``self.grads`` (same keys),
     zero at construction.  The stage enqueues on the stream that is current at
-    construction.
+    construction.  ``batch`` sequences move through the stage together (a batch
+    slice): slice tensors are then [n, batch, hidden] (token-major).
     """
 
     def __init__(self, params: List[Dict[str, torch.Tensor]], hidden: int, heads: int,
                  max_seq: int, dtype: str = "bf16", wgrad: str = "per_slice",
-                 ln_eps: float = 1e-5, device=None):
+                 ln_eps: float = 1e-5, device=None, batch: int = 1):
         self.n_layers = len(params)
         self.hidden, self.heads, self.max_seq, self.dtype = hidden, heads, max_seq, dtype
+        self.batch = batch
         self.tdtype = torch_dtype(dtype)
         self.device = torch.device(device) if device is not None else params[0]["w_qkv"].device
-        self.cfg = make_config(self.n_layers, hidden, heads, max_seq, dtype, wgrad, ln_eps)
+        self.cfg = make_config(self.n_layers, hidden, heads, max_seq, dtype, wgrad, ln_eps, batch)
         for p in params:
             for k in SYNTH_NAMES:
                 t = p[k]
@@ -194,8 +202,9 @@ class Stage:
         _check(lib.tp_kv_prefix_reset(self._h), "tp_kv_prefix_reset")
 
     def _io(self, t: torch.Tensor, n: int) -> torch.Tensor:
-        if t.dtype != self.tdtype or t.device != self.device or tuple(t.shape) != (n, self.hidden):
-            raise ValueError(f"expected a [{n}, {self.hidden}] {self.tdtype} tensor on {self.device}")
+        shape = (n, self.hidden) if self.batch == 1 else (n, self.batch, self.hidden)
+        if t.dtype != self.tdtype or t.device != self.device or tuple(t.shape) != shape:
+            raise ValueError(f"expected a {list(shape)} {self.tdtype} tensor on {self.device}")
         return t.contiguous()
 
     def forward(self, l: int, r: int, x: torch.Tensor, out: Optional[torch.Tensor] = None):
@@ -288,6 +297,41 @@ def dp_optimal_slicing(cost: np.ndarray, unit: int, K: int, eps_ns: int = 0):
                                      K, eps_ns, out, ctypes.byref(M), ctypes.byref(T)),
            "tp_dp_optimal_slicing")
     return [out[i] for i in range(M.value)], T.value
+
+
+def batch_split(T_b: Sequence[int]) -> Tuple[List[int], int]:
+    """C-ABI batch split (Sec. 3.4): T_b[b-1] = latency of a group of b
+    sequences (negative: unusable).  Returns (group sizes largest first, total)."""
+    B = len(T_b)
+    t = np.ascontiguousarray(T_b, dtype=np.int64)
+    out = (ctypes.c_int * B)()
+    D = ctypes.c_int()
+    tot = ctypes.c_int64()
+    _check(lib.tp_dp_batch_split(t.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), B, out,
+                                 ctypes.byref(D), ctypes.byref(tot)), "tp_dp_batch_split")
+    return [out[i] for i in range(D.value)], tot.value
+
+
+def joint_slicing(costs: np.ndarray, unit: int, K: int, eps_ns: int = 0):
+    """C-ABI joint batch x token plan (Sec. 3.4).  costs: int64 [B][U][U], plane
+    b-1 the cost table of a batch slice of b sequences.  Returns
+    (groups [(b, token lengths)], T_b list, total)."""
+    costs = np.ascontiguousarray(costs, dtype=np.int64)
+    B, U = costs.shape[0], costs.shape[1]
+    if costs.shape != (B, U, U):
+        raise ValueError("costs must be [B][U][U]")
+    sizes = (ctypes.c_int * B)()
+    M = (ctypes.c_int * B)()
+    lens = (ctypes.c_int * (B * U))()
+    Tb = np.zeros(B, dtype=np.int64)
+    D = ctypes.c_int()
+    tot = ctypes.c_int64()
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    _check(lib.tp_dp_joint_slicing(costs.ctypes.data_as(i64p), B, U, unit, K, eps_ns, sizes,
+                                   ctypes.byref(D), lens, M, Tb.ctypes.data_as(i64p),
+                                   ctypes.byref(tot)), "tp_dp_joint_slicing")
+    groups = [(sizes[g], [lens[g * U + i] for i in range(M[g])]) for g in range(D.value)]
+    return groups, [int(v) for v in Tb], tot.value
 
 
 def fit_ctx_model(t0: Sequence[int], unit: int, samples: Sequence[Tuple[int, int, int]]):

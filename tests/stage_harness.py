@@ -47,6 +47,48 @@ def run_oracle(params, x, dy, H, heads, L, fwd_lens, bwd_lens=None):
     return {"y": y, "dx": dx, "grads": ost.grads}
 
 
+def make_batch_inputs(n_layers, H, L, batch, dtype, seeds=(0, 1, 2), randomize_ln=False):
+    """Parameters and [L, batch, H] inputs / upstream gradients."""
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    sx, sp, sdy = seeds
+    params = synth.stage_params(n_layers, H, seed=sp, dtype=tdt, randomize_ln=randomize_ln)
+    x = synth.batch_hidden_states(L, batch, H, seed=sx, dtype=tdt)
+    dy = synth.batch_upstream_grad(L, batch, H, seed=sdy, dtype=tdt)
+    return params, x, dy
+
+
+def run_gpu_batch(params, x, dy, H, heads, L, dtype, fwd_lens, bwd_lens=None, wgrad="per_slice",
+                  device="cuda:0"):
+    """One batched stage (batch = x.shape[1]) over the whole sequence."""
+    from paper_2102_07988_amd import terapipe as tp
+    dparams = [{k: v.to(device).contiguous() for k, v in p.items()} for p in params]
+    st = tp.Stage(dparams, H, heads, L, dtype=dtype, wgrad=wgrad, batch=x.shape[1])
+    y, dx = st.run_sequence(x.to(device), dy.to(device), fwd_lens, bwd_lens)
+    torch.cuda.synchronize()
+    out = {"y": y.float().cpu().numpy(), "dx": dx.float().cpu().numpy(),
+           "grads": [{k: v.cpu().numpy() for k, v in g.items()} for g in st.grads]}
+    del st
+    return out
+
+
+def run_oracle_batch(params, x, dy, H, heads, L, fwd_lens, bwd_lens=None):
+    """The sequences of a batch are independent: one oracle run per sequence,
+    outputs stacked on axis 1, parameter gradients summed."""
+    b = x.shape[1]
+    ys, dxs, grads = [], [], None
+    for s in range(b):
+        r = run_oracle(params, x[:, s], dy[:, s], H, heads, L, fwd_lens, bwd_lens)
+        ys.append(r["y"])
+        dxs.append(r["dx"])
+        if grads is None:
+            grads = [{k: v.copy() for k, v in g.items()} for g in r["grads"]]
+        else:
+            for acc, g in zip(grads, r["grads"]):
+                for k in acc:
+                    acc[k] += g[k]
+    return {"y": np.stack(ys, axis=1), "dx": np.stack(dxs, axis=1), "grads": grads}
+
+
 def compare(got, ref, tol, label=""):
     errs = {"y": rel_l2(got["y"], ref["y"]), "dx": rel_l2(got["dx"], ref["dx"])}
     for li, (g, r) in enumerate(zip(got["grads"], ref["grads"])):

@@ -79,6 +79,21 @@ def test_workspace_size_and_init_validation():
     assert _init(tp.make_config(0, 64, 4, 32))[0] == tp.TP_ERR_INVALID
 
 
+def test_batch_config():
+    """Batch slices (Sec. 3.4): 0 means 1; the per-token arenas scale with the
+    batch (rows = max_seq * batch); sizes outside 0..64 are invalid."""
+    one = tp.workspace_bytes(tp.make_config(2, 64, 4, 32, "fp32", batch=1))
+    assert tp.workspace_bytes(tp.make_config(2, 64, 4, 32, "fp32", batch=0)) == one
+    two = tp.workspace_bytes(tp.make_config(2, 64, 4, 32, "fp32", batch=2))
+    # the same as one sequence twice as long
+    assert two == tp.workspace_bytes(tp.make_config(2, 64, 4, 64, "fp32", batch=1))
+    assert tp.workspace_bytes(tp.make_config(2, 64, 4, 32, "fp32", batch=65)) == 0
+    assert tp.workspace_bytes(tp.make_config(2, 64, 4, 32, "fp32", batch=-1)) == 0
+    rc, h = _init(tp.make_config(2, 64, 4, 32, "fp32", batch=4))
+    assert rc == tp.TP_OK
+    tp.lib.tp_stage_destroy(h)
+
+
 def test_slice_order_errors_are_host_side():
     cfg = tp.make_config(1, 64, 4, 32, "fp32")
     rc, h = _init(cfg)
