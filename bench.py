@@ -225,10 +225,41 @@ def pipeline_report(st, tp, L: int, unit: int, K: int, warmup: int, reps: int,
             "table_points": int((fcost >= 0).sum()), "profile_seconds": round(fprof_s, 2),
             "coef_ns": [round(v, 6) for v in fcoef],
             "by_K": {str(k): _slicing_summary(tp, fcost, fine_unit, k) for k in fine_K}}
+        rep["_fine_cost"] = fcost
     rep["deferred_dw_ms_per_sequence"] = round(dw_ms, 3)
     rep["note"] = ("T = Eq. 5 over t_fwd + t_bwd tables; in deferred mode the once-per-sequence "
                    "dW GEMMs (deferred_dw_ms) add to the last stage's tail and are not in t")
     return rep
+
+
+def joint_report(make_stage, tp, L: int, unit: int, K: int, B: int, cost_b1, warmup: int,
+                 reps: int):
+    """Batch x token plan of Sec. 3.4 for a batch of B sequences: the model-mode
+    cost table (Eq. 9, grid of `unit` tokens) of a stage holding b = 1..B
+    sequences per batch slice (b = 1: `cost_b1`), the optimal token slicing and
+    latency T_b of each group size, and the group sizes chosen by the batch
+    split (knapsack over T_b), next to B single sequences and one group of B."""
+    import numpy as np
+    U = L // unit
+    ks, js = _subset(U)
+    costs = np.zeros((B, U, U), dtype=np.int64)
+    costs[0] = cost_b1
+    prof_s = 0.0
+    for b in range(2, B + 1):
+        stb = make_stage(b)
+        t0 = time.perf_counter()
+        costs[b - 1], _ = stb.profile_model(L, unit, [unit * k for k in ks],
+                                            [unit * j for j in js], warmup=warmup, reps=reps)
+        prof_s += time.perf_counter() - t0
+        del stb
+    groups, T_b, total = tp.joint_slicing(costs, unit, K)
+    return {"B": B, "unit": unit, "K": K, "profile_seconds": round(prof_s, 2),
+            "T_b_ms": [round(t / 1e6, 3) for t in T_b],
+            "T_b_per_sequence_ms": [round(t / (b + 1) / 1e6, 3) for b, t in enumerate(T_b)],
+            "groups": [{"sequences": b, "slicing": sl} for b, sl in groups],
+            "total_ms": round(total / 1e6, 3),
+            "all_single_sequences_ms": round(B * T_b[0] / 1e6, 3),
+            "one_group_ms": round(T_b[B - 1] / 1e6, 3)}
 
 
 def main():
@@ -253,6 +284,10 @@ def main():
     ap.add_argument("--pipeline-fine-unit", type=int, default=16,
                     help="grid of the model-mode (Eq. 9) table for the uniform-vs-DP sweep; "
                          "0 skips it")
+    ap.add_argument("--joint-batch", type=int, default=2,
+                    help="batch size B of the Sec. 3.4 batch x token plan in the pipeline "
+                         "report (model-mode tables for 1..B sequences per batch slice); "
+                         "0 or 1 skips it")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (4 times), for "
                          "scaling the HBM byte counters")
@@ -437,9 +472,16 @@ def main():
             torch.cuda.synchronize()
             return (time.perf_counter() - ta) * 1e3 / reps
 
-        out["pipeline"] = pipeline_report(st, tp, L, args.pipeline_unit, args.pipeline_K, 1, 3,
-                                          run_slicing, dw_ms, args.pipeline_fine_unit, n_layers, H,
-                                          args.wgrad == "deferred")
+        rep = pipeline_report(st, tp, L, args.pipeline_unit, args.pipeline_K, 1, 3,
+                              run_slicing, dw_ms, args.pipeline_fine_unit, n_layers, H,
+                              args.wgrad == "deferred")
+        fine_cost = rep.pop("_fine_cost", None)
+        if args.joint_batch >= 2 and fine_cost is not None:
+            rep["joint"] = joint_report(
+                lambda b: tp.Stage(params, H, heads, L, dtype="bf16", wgrad=args.wgrad, batch=b),
+                tp, L, args.pipeline_fine_unit, PAPER_K[args.workload], args.joint_batch,
+                fine_cost, 1, 3)
+        out["pipeline"] = rep
         st.zero_grads()
     out["mfma_probe_tflops"] = round(tp.measure_mfma_peak(), 1)
     if not args.no_cpu_baseline:
