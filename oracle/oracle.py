@@ -53,6 +53,10 @@ def load_library():
         lib.or_stage_create.restype = ctypes.c_void_p
         lib.or_stage_create.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                         ctypes.c_double, ctypes.c_void_p, ctypes.c_void_p]
+        lib.or_stage_create_ex.restype = ctypes.c_void_p
+        lib.or_stage_create_ex.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                           ctypes.c_int, ctypes.c_int, ctypes.c_double,
+                                           ctypes.c_void_p, ctypes.c_void_p]
         lib.or_stage_destroy.argtypes = [ctypes.c_void_p]
         lib.or_reset.argtypes = [ctypes.c_void_p]
         lib.or_forward.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, _DP, _DP]
@@ -91,14 +95,22 @@ class OracleStage:
     ``params`` is a list (one dict per layer) of arrays named by PARAM_NAMES,
     weights stored [out, in]; they are converted to float64 and kept alive.
     Gradients accumulate into ``self.grads`` (same structure, float64, zeroed at
-    construction and by ``zero_grads``).
+    construction and by ``zero_grads``).  ``op_parts`` p > 1 makes the stage one
+    device's shard of p-way operation partitioning: heads / p heads and 4H / p
+    FFN units (weights of the shard's shapes), the output and FC2 projections'
+    partial sums taken as the whole sum.
     """
 
     def __init__(self, params: List[Dict[str, np.ndarray]], hidden: int, heads: int,
-                 max_seq: int, eps: float = 1e-5):
+                 max_seq: int, eps: float = 1e-5, op_parts: int = 1):
         self._lib = load_library()
         self.n_layers = len(params)
         self.hidden, self.heads, self.max_seq = hidden, heads, max_seq
+        if heads % op_parts or (4 * hidden) % op_parts or hidden % heads:
+            raise ValueError("invalid operation partitioning")
+        self.op_parts = op_parts
+        self.d = hidden // heads
+        self.attn_width = heads // op_parts * self.d
         self.params = [{k: np.ascontiguousarray(np.asarray(p[k], dtype=np.float64))
                         for k in PARAM_NAMES} for p in params]
         self.grads = [{k: np.zeros_like(v) for k, v in p.items()} for p in self.params]
@@ -108,9 +120,10 @@ class OracleStage:
             for k in PARAM_NAMES:
                 setattr(self._p_structs[i], k, _ptr(self.params[i][k]))
                 setattr(self._g_structs[i], k, _ptr(self.grads[i][k]))
-        self._h = self._lib.or_stage_create(self.n_layers, hidden, heads, max_seq, eps,
-                                            ctypes.addressof(self._p_structs),
-                                            ctypes.addressof(self._g_structs))
+        self._h = self._lib.or_stage_create_ex(self.n_layers, hidden, heads // op_parts, self.d,
+                                               4 * hidden // op_parts, max_seq, eps,
+                                               ctypes.addressof(self._p_structs),
+                                               ctypes.addressof(self._g_structs))
         if not self._h:
             raise ValueError("invalid oracle stage configuration")
 
@@ -159,7 +172,7 @@ class OracleStage:
 
     def cache(self, layer: int, which: str) -> np.ndarray:
         idx = {"k": 0, "v": 1, "dk": 2, "dv": 3}[which]
-        out = np.zeros((self.max_seq, self.hidden))
+        out = np.zeros((self.max_seq, self.attn_width))
         n = self._lib.or_get_cache(self._h, layer, idx, _ptr(out))
         return out[:n].copy()
 

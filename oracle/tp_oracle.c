@@ -25,6 +25,12 @@
  *   u2 = LN2(x1);  z = W_1 u2 + b_1;  g = GELU(z)
  *   y  = x1 + W_2 g + b_2
  *
+ * A stage may also be one device's shard of operation partitioning (the #Op
+ * column of Table 1, partitioning inside a layer as in Megatron-LM): heads / p
+ * heads and 4H / p FFN units; the partial sums of the output and FC2
+ * projections that the all-reduce would add up across devices are taken as this
+ * device's whole sum (or_stage_create_ex).
+ *
  * Slices (Sec. 3.2): a forward call processes tokens [l, r) with l equal to the
  * number of tokens already cached, attending to the cached K/V of every earlier
  * slice.  Backward calls run slices in reverse order; the gradient flowing into
@@ -65,13 +71,13 @@ typedef struct {
 /* Per-layer state; every per-token array is indexed by absolute position. */
 typedef struct {
   double *x, *mean1, *rstd1, *u, *q, *o, *x1, *mean2, *rstd2, *u2, *z, *g;
-  double *kc, *vc;   /* K/V cache [Lmax][H] */
-  double *dk, *dv;   /* dK/dV gradient buffer [Lmax][H] */
-  double *dx1, *dob; /* backward temporaries [Lmax][H] */
+  double *kc, *vc;   /* K/V cache [Lmax][A] */
+  double *dk, *dv;   /* dK/dV gradient buffer [Lmax][A] */
+  double *dx1, *dob; /* backward temporaries [Lmax][H], [Lmax][A] */
 } or_layer_state;
 
 typedef struct {
-  int n_layers, H, heads, d, F, Lmax;
+  int n_layers, H, heads, d, A, F, Lmax; /* A = heads * d (attention width), F = FFN width */
   double eps;
   int cached_len, bwd_frontier;
   const or_params *p;
@@ -171,12 +177,12 @@ static void ln_row_bwd(int H, const double *x, double mean, double rstd, const d
 
 /* Softmax weights of query t of head h over keys 0..t (Eq. 2): fills P[0..t]. */
 static void attn_probs(const or_stage *S, const or_layer_state *L, int t, int h, double *P) {
-  const int H = S->H, d = S->d;
+  const int A = S->A, d = S->d;
   const double scale = 1.0 / sqrt((double)d);
-  const double *q = L->q + (size_t)t * H + h * d;
+  const double *q = L->q + (size_t)t * A + h * d;
   double mx = -INFINITY;
   for (int s = 0; s <= t; ++s) {
-    const double *k = L->kc + (size_t)s * H + h * d;
+    const double *k = L->kc + (size_t)s * A + h * d;
     double dot = 0.0;
     for (int j = 0; j < d; ++j) dot += q[j] * k[j];
     P[s] = dot * scale;
@@ -192,43 +198,56 @@ static void attn_probs(const or_stage *S, const or_layer_state *L, int t, int h,
 
 /* ----------------------------------------------------------------- the stage */
 
-or_stage *or_stage_create(int n_layers, int H, int heads, int Lmax, double eps,
-                          const or_params *p, or_grads *g) {
-  if (n_layers < 1 || H < 1 || heads < 1 || H % heads || Lmax < 1 || !p || !g) return NULL;
+/* A stage whose attention has `heads` heads of width d and whose FFN has F
+ * units, on a residual stream of width H (the full block: heads * d = H,
+ * F = 4H; one GPU's shard of p-way operation partitioning: heads / p heads and
+ * 4H / p units, the partial sums of the output and FC2 projections taken as
+ * this device's whole sum). */
+or_stage *or_stage_create_ex(int n_layers, int H, int heads, int d, int F, int Lmax, double eps,
+                             const or_params *p, or_grads *g) {
+  if (n_layers < 1 || H < 1 || heads < 1 || d < 1 || F < 1 || Lmax < 1 || !p || !g) return NULL;
   or_stage *S = (or_stage *)calloc(1, sizeof(or_stage));
   S->n_layers = n_layers;
   S->H = H;
   S->heads = heads;
-  S->d = H / heads;
-  S->F = 4 * H;
+  S->d = d;
+  S->A = heads * d;
+  S->F = F;
   S->Lmax = Lmax;
   S->eps = eps;
   S->p = p;
   S->gr = g;
   S->st = (or_layer_state *)calloc(n_layers, sizeof(or_layer_state));
-  const size_t LH = (size_t)Lmax * H, LF = (size_t)Lmax * S->F;
+  const size_t LH = (size_t)Lmax * H, LF = (size_t)Lmax * S->F, LA = (size_t)Lmax * S->A;
   for (int i = 0; i < n_layers; ++i) {
     or_layer_state *L = &S->st[i];
     L->x = zalloc(LH);
     L->mean1 = zalloc(Lmax);
     L->rstd1 = zalloc(Lmax);
     L->u = zalloc(LH);
-    L->q = zalloc(LH);
-    L->o = zalloc(LH);
+    L->q = zalloc(LA);
+    L->o = zalloc(LA);
     L->x1 = zalloc(LH);
     L->mean2 = zalloc(Lmax);
     L->rstd2 = zalloc(Lmax);
     L->u2 = zalloc(LH);
     L->z = zalloc(LF);
     L->g = zalloc(LF);
-    L->kc = zalloc(LH);
-    L->vc = zalloc(LH);
-    L->dk = zalloc(LH);
-    L->dv = zalloc(LH);
+    L->kc = zalloc(LA);
+    L->vc = zalloc(LA);
+    L->dk = zalloc(LA);
+    L->dv = zalloc(LA);
     L->dx1 = zalloc(LH);
-    L->dob = zalloc(LH);
+    L->dob = zalloc(LA);
   }
   return S;
+}
+
+/* The full block: heads of width H / heads, FFN width 4H. */
+or_stage *or_stage_create(int n_layers, int H, int heads, int Lmax, double eps,
+                          const or_params *p, or_grads *g) {
+  if (heads < 1 || H % heads) return NULL;
+  return or_stage_create_ex(n_layers, H, heads, H / heads, 4 * H, Lmax, eps, p, g);
 }
 
 void or_stage_destroy(or_stage *S) {
@@ -247,10 +266,10 @@ void or_stage_destroy(or_stage *S) {
 void or_reset(or_stage *S) {
   S->cached_len = 0;
   S->bwd_frontier = 0;
-  const size_t LH = (size_t)S->Lmax * S->H;
+  const size_t LA = (size_t)S->Lmax * S->A;
   for (int i = 0; i < S->n_layers; ++i) {
-    memset(S->st[i].dk, 0, LH * sizeof(double));
-    memset(S->st[i].dv, 0, LH * sizeof(double));
+    memset(S->st[i].dk, 0, LA * sizeof(double));
+    memset(S->st[i].dv, 0, LA * sizeof(double));
   }
 }
 
@@ -258,8 +277,8 @@ void or_reset(or_stage *S) {
 int or_forward(or_stage *S, int l, int r, const double *x, double *y) {
   if (!S || !x || !y || l < 0 || r <= l || r > S->Lmax) return OR_ERR_INVALID;
   if (l != S->cached_len) return OR_ERR_ORDER;
-  const int H = S->H, F = S->F, a = S->heads, d = S->d, n = r - l;
-  double *qkv = zalloc((size_t)n * 3 * H);
+  const int H = S->H, A = S->A, F = S->F, a = S->heads, d = S->d, n = r - l;
+  double *qkv = zalloc((size_t)n * 3 * A);
   double *tmp = zalloc((size_t)n * H);
   for (int li = 0; li < S->n_layers; ++li) {
     const or_params *p = &S->p[li];
@@ -276,11 +295,11 @@ int or_forward(or_stage *S, int l, int r, const double *x, double *y) {
     for (int t = l; t < r; ++t)
       ln_row(H, S->eps, L->x + (size_t)t * H, p->ln1_g, p->ln1_b, L->u + (size_t)t * H,
              &L->mean1[t], &L->rstd1[t]);
-    mm_nt_bias(n, 3 * H, H, L->u + (size_t)l * H, p->w_qkv, p->b_qkv, qkv);
+    mm_nt_bias(n, 3 * A, H, L->u + (size_t)l * H, p->w_qkv, p->b_qkv, qkv);
     for (int t = 0; t < n; ++t) {
-      memcpy(L->q + (size_t)(l + t) * H, qkv + (size_t)t * 3 * H, H * sizeof(double));
-      memcpy(L->kc + (size_t)(l + t) * H, qkv + (size_t)t * 3 * H + H, H * sizeof(double));
-      memcpy(L->vc + (size_t)(l + t) * H, qkv + (size_t)t * 3 * H + 2 * H, H * sizeof(double));
+      memcpy(L->q + (size_t)(l + t) * A, qkv + (size_t)t * 3 * A, A * sizeof(double));
+      memcpy(L->kc + (size_t)(l + t) * A, qkv + (size_t)t * 3 * A + A, A * sizeof(double));
+      memcpy(L->vc + (size_t)(l + t) * A, qkv + (size_t)t * 3 * A + 2 * A, A * sizeof(double));
     }
     /* attention: each query row of each head over keys 0..t */
 #pragma omp parallel if ((long)n * a * r * d > 200000)
@@ -290,16 +309,16 @@ int or_forward(or_stage *S, int l, int r, const double *x, double *y) {
       for (int t = l; t < r; ++t)
         for (int h = 0; h < a; ++h) {
           attn_probs(S, L, t, h, Pl);
-          double *o = L->o + (size_t)t * H + h * d;
+          double *o = L->o + (size_t)t * A + h * d;
           for (int j = 0; j < d; ++j) {
             double acc = 0.0;
-            for (int s = 0; s <= t; ++s) acc += Pl[s] * L->vc[(size_t)s * H + h * d + j];
+            for (int s = 0; s <= t; ++s) acc += Pl[s] * L->vc[(size_t)s * A + h * d + j];
             o[j] = acc;
           }
         }
       free(Pl);
     }
-    mm_nt_bias(n, H, H, L->o + (size_t)l * H, p->w_o, p->b_o, L->x1 + (size_t)l * H);
+    mm_nt_bias(n, H, A, L->o + (size_t)l * A, p->w_o, p->b_o, L->x1 + (size_t)l * H);
     for (size_t i = 0; i < (size_t)n * H; ++i) L->x1[(size_t)l * H + i] += L->x[(size_t)l * H + i];
     for (int t = l; t < r; ++t)
       ln_row(H, S->eps, L->x1 + (size_t)t * H, p->ln2_g, p->ln2_b, L->u2 + (size_t)t * H,
@@ -325,16 +344,16 @@ int or_forward(or_stage *S, int l, int r, const double *x, double *y) {
 int or_backward(or_stage *S, int l, int r, const double *dy, double *dx) {
   if (!S || !dy || !dx || l < 0 || r <= l || r > S->Lmax) return OR_ERR_INVALID;
   if (r != S->bwd_frontier) return OR_ERR_ORDER;
-  const int H = S->H, F = S->F, a = S->heads, d = S->d, n = r - l;
+  const int H = S->H, A = S->A, F = S->F, a = S->heads, d = S->d, n = r - l;
   const double scale = 1.0 / sqrt((double)d);
   double *dcur = zalloc((size_t)n * H); /* gradient w.r.t. this layer's output, rows [l,r) */
   memcpy(dcur, dy, (size_t)n * H * sizeof(double));
   double *dg = zalloc((size_t)n * F), *dz = zalloc((size_t)n * F);
-  double *du2 = zalloc((size_t)n * H), *dq = zalloc((size_t)n * H);
-  double *dqkv = zalloc((size_t)n * 3 * H), *du = zalloc((size_t)n * H);
+  double *du2 = zalloc((size_t)n * H), *dq = zalloc((size_t)n * A);
+  double *dqkv = zalloc((size_t)n * 3 * A), *du = zalloc((size_t)n * H);
   double *dyabs = zalloc((size_t)S->Lmax * H);
   double *dzabs = zalloc((size_t)S->Lmax * F);
-  double *dqkvabs = zalloc((size_t)S->Lmax * 3 * H);
+  double *dqkvabs = zalloc((size_t)S->Lmax * 3 * A);
   for (int li = S->n_layers - 1; li >= 0; --li) {
     const or_params *p = &S->p[li];
     or_grads *G = &S->gr[li];
@@ -361,8 +380,8 @@ int or_backward(or_stage *S, int l, int r, const double *dy, double *dx) {
       for (int i = 0; i < H; ++i) dx1[i] += dcur[(size_t)(t - l) * H + i];
     }
     /* output projection: x1 = x + W_o o + b_o */
-    acc_wgrad_desc(l, r, H, H, L->dx1, L->o, G->w_o, G->b_o);
-    mm_nn(n, H, H, L->dx1 + (size_t)l * H, p->w_o, L->dob + (size_t)l * H);
+    acc_wgrad_desc(l, r, H, A, L->dx1, L->o, G->w_o, G->b_o);
+    mm_nn(n, A, H, L->dx1 + (size_t)l * H, p->w_o, L->dob + (size_t)l * A);
     /* attention backward: dq rows; dK/dV buffer for keys 0..t, queries descending */
 #pragma omp parallel if ((long)n * a * r * d > 200000)
     {
@@ -371,23 +390,23 @@ int or_backward(or_stage *S, int l, int r, const double *dy, double *dx) {
       for (int h = 0; h < a; ++h)
         for (int t = r - 1; t >= l; --t) {
           attn_probs(S, L, t, h, Pl);
-          const double *dob = L->dob + (size_t)t * H + h * d;
-          const double *q = L->q + (size_t)t * H + h * d;
+          const double *dob = L->dob + (size_t)t * A + h * d;
+          const double *q = L->q + (size_t)t * A + h * d;
           double D = 0.0;
           for (int s = 0; s <= t; ++s) {
-            const double *v = L->vc + (size_t)s * H + h * d;
+            const double *v = L->vc + (size_t)s * A + h * d;
             double acc = 0.0;
             for (int j = 0; j < d; ++j) acc += dob[j] * v[j];
             dP[s] = acc;
             D += Pl[s] * acc;
           }
-          double *dqt = dq + (size_t)(t - l) * H + h * d;
+          double *dqt = dq + (size_t)(t - l) * A + h * d;
           for (int j = 0; j < d; ++j) dqt[j] = 0.0;
           for (int s = 0; s <= t; ++s) {
             const double dS = Pl[s] * (dP[s] - D);
-            const double *k = L->kc + (size_t)s * H + h * d;
-            double *dkr = L->dk + (size_t)s * H + h * d;
-            double *dvr = L->dv + (size_t)s * H + h * d;
+            const double *k = L->kc + (size_t)s * A + h * d;
+            double *dkr = L->dk + (size_t)s * A + h * d;
+            double *dvr = L->dv + (size_t)s * A + h * d;
             for (int j = 0; j < d; ++j) {
               dqt[j] += dS * k[j] * scale;
               dkr[j] += dS * q[j] * scale;
@@ -400,13 +419,13 @@ int or_backward(or_stage *S, int l, int r, const double *dy, double *dx) {
     }
     /* QKV projection: keys/values of [l, r) are complete in the buffer now */
     for (int t = 0; t < n; ++t) {
-      memcpy(dqkv + (size_t)t * 3 * H, dq + (size_t)t * H, H * sizeof(double));
-      memcpy(dqkv + (size_t)t * 3 * H + H, L->dk + (size_t)(l + t) * H, H * sizeof(double));
-      memcpy(dqkv + (size_t)t * 3 * H + 2 * H, L->dv + (size_t)(l + t) * H, H * sizeof(double));
+      memcpy(dqkv + (size_t)t * 3 * A, dq + (size_t)t * A, A * sizeof(double));
+      memcpy(dqkv + (size_t)t * 3 * A + A, L->dk + (size_t)(l + t) * A, A * sizeof(double));
+      memcpy(dqkv + (size_t)t * 3 * A + 2 * A, L->dv + (size_t)(l + t) * A, A * sizeof(double));
     }
-    memcpy(dqkvabs + (size_t)l * 3 * H, dqkv, (size_t)n * 3 * H * sizeof(double));
-    acc_wgrad_desc(l, r, 3 * H, H, dqkvabs, L->u, G->w_qkv, G->b_qkv);
-    mm_nn(n, H, 3 * H, dqkv, p->w_qkv, du);
+    memcpy(dqkvabs + (size_t)l * 3 * A, dqkv, (size_t)n * 3 * A * sizeof(double));
+    acc_wgrad_desc(l, r, 3 * A, H, dqkvabs, L->u, G->w_qkv, G->b_qkv);
+    mm_nn(n, H, 3 * A, dqkv, p->w_qkv, du);
     /* LN1 and the residual: dx = dx1 + LN1^T(du) */
     for (int t = r - 1; t >= l; --t) {
       const double *xr = L->x + (size_t)t * H;
@@ -442,7 +461,7 @@ int or_get_cache(const or_stage *S, int layer, int which, double *out) {
   if (!S || layer < 0 || layer >= S->n_layers || which < 0 || which > 3) return OR_ERR_INVALID;
   const or_layer_state *L = &S->st[layer];
   const double *src = which == 0 ? L->kc : which == 1 ? L->vc : which == 2 ? L->dk : L->dv;
-  memcpy(out, src, (size_t)S->cached_len * S->H * sizeof(double));
+  memcpy(out, src, (size_t)S->cached_len * S->A * sizeof(double));
   return S->cached_len;
 }
 

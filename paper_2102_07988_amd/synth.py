@@ -25,10 +25,12 @@ PARAM_NAMES = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
 SEED_X, SEED_PARAMS, SEED_DY = 0, 1, 2
 
 
-def param_shapes(hidden: int) -> Dict[str, tuple]:
-    H, F = hidden, 4 * hidden
-    return {"ln1_g": (H,), "ln1_b": (H,), "w_qkv": (3 * H, H), "b_qkv": (3 * H,),
-            "w_o": (H, H), "b_o": (H,), "ln2_g": (H,), "ln2_b": (H,),
+def param_shapes(hidden: int, op_parts: int = 1) -> Dict[str, tuple]:
+    """Parameter shapes of one layer; op_parts p > 1: one device's shard of
+    p-way operation partitioning (attention width H / p, FFN width 4H / p)."""
+    H, A, F = hidden, hidden // op_parts, 4 * hidden // op_parts
+    return {"ln1_g": (H,), "ln1_b": (H,), "w_qkv": (3 * A, H), "b_qkv": (3 * A,),
+            "w_o": (H, A), "b_o": (H,), "ln2_g": (H,), "ln2_b": (H,),
             "w1": (F, H), "b1": (F,), "w2": (H, F), "b2": (H,)}
 
 
@@ -51,8 +53,8 @@ def normal(shape, seed: int, stream: int, std: float = 1.0, mean: float = 0.0,
 
 def stage_params(n_layers: int, hidden: int, seed: int = SEED_PARAMS, dtype=torch.float32,
                  device="cpu", randomize_ln: bool = False,
-                 weight_std: float = 0.02) -> List[Dict[str, torch.Tensor]]:
-    shapes = param_shapes(hidden)
+                 weight_std: float = 0.02, op_parts: int = 1) -> List[Dict[str, torch.Tensor]]:
+    shapes = param_shapes(hidden, op_parts)
     layers = []
     for li in range(n_layers):
         p = {}
