@@ -75,12 +75,19 @@ typedef struct {
                      (Sec. 3.4, slicing the batch and token dimensions jointly); 0 means 1,
                      at most 64.  Token t of sequence s is row t * b + s of every
                      slice tensor below, so a slice [l, r) is (r-l) * b consecutive rows. */
+  int op_parts;   /* p: the stage is one device's shard of p-way operation partitioning
+                     inside each layer (the #Op column of Table 1): heads / p heads and
+                     4H / p FFN units on the full residual stream, the output and FC2
+                     projections' partial sums taken as this device's whole sum (the
+                     all-reduce across the p devices is left out).  0 means 1; heads and
+                     4H must be multiples of p.  Weight shapes below use A = H / p and
+                     F = 4H / p (A = H, F = 4H for p = 1). */
 } tp_stage_config;
 
-/* Parameters (stage dtype) or gradients (fp32) of one layer.  Shapes:
- * ln*_g, ln*_b, b_o, b_fc2: [H]; w_qkv: [3H][H] (rows: q, then k, then v;
- * head h owns rows h*d..h*d+d-1 of each); b_qkv: [3H]; w_o: [H][H];
- * w_fc1: [4H][H]; b_fc1: [4H]; w_fc2: [H][4H]. */
+/* Parameters (stage dtype) or gradients (fp32) of one layer.  Shapes (A and F
+ * as in tp_stage_config.op_parts): ln*_g, ln*_b, b_o, b_fc2: [H]; w_qkv: [3A][H]
+ * (rows: q, then k, then v; local head h owns rows h*d..h*d+d-1 of each);
+ * b_qkv: [3A]; w_o: [H][A]; w_fc1: [F][H]; b_fc1: [F]; w_fc2: [H][F]. */
 typedef struct {
   void *ln1_g, *ln1_b, *w_qkv, *b_qkv, *w_o, *b_o;
   void *ln2_g, *ln2_b, *w_fc1, *b_fc1, *w_fc2, *b_fc2;

@@ -62,7 +62,9 @@ struct PendingTiming {
 
 struct tp_stage {
   tp_stage_config cfg;
-  int H, F, heads, d, L, dt;
+  // H: residual width; A = heads * d: attention width of this device's heads;
+  // F: its FFN width (A = H, F = 4H without operation partitioning)
+  int H, A, F, heads, d, L, dt;
   int bsz;  // sequences per batch slice: token t of sequence s is row t * bsz + s
   size_t esz;
   std::vector<tp_layer_ptrs> P, G;
@@ -90,10 +92,13 @@ bool config_ok(const tp_stage_config* c) {
   if (c->wgrad_mode != TP_WGRAD_PER_SLICE && c->wgrad_mode != TP_WGRAD_DEFERRED) return false;
   if (!(c->ln_eps > 0.f) || !std::isfinite(c->ln_eps)) return false;
   if (c->batch < 0 || c->batch > 64) return false;
+  const int p = c->op_parts > 0 ? c->op_parts : 1;
+  if (c->op_parts < 0 || c->heads % p || (4 * c->hidden) % p) return false;
   return true;
 }
 
 int batch_of(const tp_stage_config* c) { return c->batch > 0 ? c->batch : 1; }
+int parts_of(const tp_stage_config* c) { return c->op_parts > 0 ? c->op_parts : 1; }
 
 bool config_supported(const tp_stage_config* c) {
   const int d = c->hidden / c->heads;
@@ -108,15 +113,16 @@ size_t carve(const tp_stage_config* c, void* base, std::vector<LayerBufs>* lbs, 
   Carver cv(base);
   const size_t esz = c->dtype == TP_DTYPE_FP32 ? 4 : 2;
   // every per-token arena holds max_seq * batch rows
-  const size_t L = (size_t)c->max_seq * batch_of(c), H = c->hidden, F = 4 * H, a = c->heads;
+  const size_t L = (size_t)c->max_seq * batch_of(c), H = c->hidden, pp = parts_of(c);
+  const size_t a = c->heads / pp, A = a * (H / c->heads), F = 4 * H / pp;
   for (int i = 0; i < c->n_layers; ++i) {
     LayerBufs b;
     b.x_in = cv.take(L * H * esz);
     b.u = cv.take(L * H * esz);
-    b.q = cv.take(L * H * esz);
-    b.kc = cv.take(L * H * esz);
-    b.vc = cv.take(L * H * esz);
-    b.o = cv.take(L * H * esz);
+    b.q = cv.take(L * A * esz);
+    b.kc = cv.take(L * A * esz);
+    b.vc = cv.take(L * A * esz);
+    b.o = cv.take(L * A * esz);
     b.x1 = cv.take(L * H * esz);
     b.u2 = cv.take(L * H * esz);
     b.z = cv.take(L * F * esz);
@@ -126,23 +132,23 @@ size_t carve(const tp_stage_config* c, void* base, std::vector<LayerBufs>* lbs, 
     b.mean2 = (float*)cv.take(L * 4);
     b.rstd2 = (float*)cv.take(L * 4);
     b.lse = (float*)cv.take(a * L * 4);
-    b.dk = (float*)cv.take(L * H * 4);
-    b.dv = (float*)cv.take(L * H * 4);
+    b.dk = (float*)cv.take(L * A * 4);
+    b.dv = (float*)cv.take(L * A * 4);
     b.dy = cv.take(L * H * esz);
     b.dz = cv.take(L * F * esz);
     b.dx1 = cv.take(L * H * esz);
-    b.dqkv = cv.take(L * 3 * H * esz);
+    b.dqkv = cv.take(L * 3 * A * esz);
     if (lbs) lbs->push_back(b);
   }
   Scratch s;
   s.du2 = cv.take(L * H * esz);
   s.du = cv.take(L * H * esz);
-  s.dout = cv.take(L * H * esz);
+  s.dout = cv.take(L * A * esz);
   s.D = (float*)cv.take(a * L * 4);
   s.io_a = cv.take(L * H * esz);
   s.io_b = cv.take(L * H * esz);
-  // up to 8 partial [min(L, 256)][4H] fp32 products
-  s.splitk_elems = 8 * std::min<size_t>(L, 256) * F;
+  // up to 8 partial [min(L, 256)][widest product output] fp32 products
+  s.splitk_elems = 8 * std::min<size_t>(L, 256) * std::max(std::max(F, H), 3 * A);
   s.splitk = (float*)cv.take(s.splitk_elems * 4);
   if (sc) *sc = s;
   return (cv.off + 255) & ~(size_t)255;
@@ -229,7 +235,7 @@ GemmArgs tn(int M, int N, int K, const void* dY, long ldy, const void* X, long l
 
 // rows [l, l + n) of the per-token arenas
 tp_status wgrad_gemms(tp_stage* S, int li, int l, int n) {
-  const int H = S->H, F = S->F;
+  const int H = S->H, A = S->A, F = S->F;
   const size_t e = S->esz;
   LayerBufs& B = S->lb[li];
   tp_layer_ptrs& G = S->G[li];
@@ -237,15 +243,15 @@ tp_status wgrad_gemms(tp_stage* S, int li, int l, int n) {
                                 (float*)G.w_fc2)));
   TRY(run_gemm(S, K_GEMM_DW, tn(F, H, n, rowp(B.dz, l, F, e), F, rowp(B.u2, l, H, e), H,
                                 (float*)G.w_fc1)));
-  TRY(run_gemm(S, K_GEMM_DW, tn(H, H, n, rowp(B.dx1, l, H, e), H, rowp(B.o, l, H, e), H,
+  TRY(run_gemm(S, K_GEMM_DW, tn(H, A, n, rowp(B.dx1, l, H, e), H, rowp(B.o, l, A, e), A,
                                 (float*)G.w_o)));
-  TRY(run_gemm(S, K_GEMM_DW, tn(3 * H, H, n, rowp(B.dqkv, l, 3 * H, e), 3 * H,
+  TRY(run_gemm(S, K_GEMM_DW, tn(3 * A, H, n, rowp(B.dqkv, l, 3 * A, e), 3 * A,
                                 rowp(B.u, l, H, e), H, (float*)G.w_qkv)));
   return TP_OK;
 }
 
 tp_status forward_impl(tp_stage* S, int l, int r, const void* x, void* y) {
-  const int H = S->H, F = S->F, NL = S->cfg.n_layers, dt = S->dt;
+  const int H = S->H, A = S->A, F = S->F, NL = S->cfg.n_layers, dt = S->dt;
   // batch slice: tokens [l, r) of bsz sequences are rows [lr, lr + n)
   const int ntok = r - l, lr = l * S->bsz, n = ntok * S->bsz;
   const size_t e = S->esz;
@@ -259,20 +265,20 @@ tp_status forward_impl(tp_stage* S, int l, int r, const void* x, void* y) {
       return ln_fwd(dt, n, H, li == 0 ? x : xin, li == 0 ? xin : nullptr, P.ln1_g, P.ln1_b,
                     rowp(B.u, lr, H, e), B.mean1 + lr, B.rstd1 + lr, S->cfg.ln_eps, st);
     }));
-    GemmArgs g = nt(n, 3 * H, H, rowp(B.u, lr, H, e), H, P.w_qkv);
+    GemmArgs g = nt(n, 3 * A, H, rowp(B.u, lr, H, e), H, P.w_qkv);
     g.epi = EPI_QKV;
     g.bias = P.b_qkv;
-    g.q = rowp(B.q, lr, H, e), g.k = rowp(B.kc, lr, H, e), g.v = rowp(B.vc, lr, H, e), g.H = H;
+    g.q = rowp(B.q, lr, A, e), g.k = rowp(B.kc, lr, A, e), g.v = rowp(B.vc, lr, A, e), g.H = A;
     TRY(run_gemm(S, K_GEMM_FWD, g));
     AttnArgs a;
-    a.l = l, a.r = r, a.H = H, a.heads = S->heads, a.d = S->d, a.Lmax = S->L;
-    a.bs = S->bsz, a.ld = S->bsz * H;
+    a.l = l, a.r = r, a.H = A, a.heads = S->heads, a.d = S->d, a.Lmax = S->L;
+    a.bs = S->bsz, a.ld = S->bsz * A;
     a.scale = 1.f / std::sqrt((float)S->d);
-    a.q = rowp(B.q, lr, H, e), a.kc = B.kc, a.vc = B.vc, a.o = rowp(B.o, lr, H, e), a.lse = B.lse;
+    a.q = rowp(B.q, lr, A, e), a.kc = B.kc, a.vc = B.vc, a.o = rowp(B.o, lr, A, e), a.lse = B.lse;
     const double pairs = ((double)ntok * l + (double)ntok * (ntok + 1) / 2) * S->bsz;
-    TRY(launch(S, K_ATTN_FWD, 4.0 * H * pairs, (2.0 * ntok + 2.0 * r) * S->bsz * H * e,
+    TRY(launch(S, K_ATTN_FWD, 4.0 * A * pairs, (2.0 * ntok + 2.0 * r) * S->bsz * A * e,
                [&] { return attn_fwd(dt, a, st); }));
-    g = nt(n, H, H, rowp(B.o, lr, H, e), H, P.w_o);
+    g = nt(n, H, A, rowp(B.o, lr, A, e), A, P.w_o);
     g.epi = EPI_RESID, g.bias = P.b_o, g.R = xin, g.ldr = H, g.C = rowp(B.x1, lr, H, e), g.ldc = H;
     TRY(run_gemm(S, K_GEMM_FWD, g));
     TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
@@ -292,7 +298,7 @@ tp_status forward_impl(tp_stage* S, int l, int r, const void* x, void* y) {
 }
 
 tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
-  const int H = S->H, F = S->F, NL = S->cfg.n_layers, dt = S->dt;
+  const int H = S->H, A = S->A, F = S->F, NL = S->cfg.n_layers, dt = S->dt;
   // batch slice: tokens [l, r) of bsz sequences are rows [lr, lr + n)
   const int ntok = r - l, lr = l * S->bsz, n = ntok * S->bsz;
   const size_t e = S->esz;
@@ -328,35 +334,35 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
                             (float*)G.ln2_g, (float*)G.ln2_b, st);
     }));
     // output projection backward: dO = dx1 W_o
-    g = nn(n, H, H, rowp(B.dx1, lr, H, e), H, P.w_o);
-    g.C = S->sc.dout, g.ldc = H;
+    g = nn(n, A, H, rowp(B.dx1, lr, H, e), H, P.w_o);
+    g.C = S->sc.dout, g.ldc = A;
     TRY(run_gemm(S, K_GEMM_DX, g));
     TRY(launch(S, K_MISC, 0, nb, [&] {
       return colsum_acc(dt, n, H, rowp(B.dx1, lr, H, e), H, (float*)G.b_o, st);
     }));
     // attention backward: dq rows, dK/dV into the fp32 buffer for keys [0, r)
     AttnArgs a;
-    a.l = l, a.r = r, a.H = H, a.heads = S->heads, a.d = S->d, a.Lmax = S->L;
-    a.bs = S->bsz, a.ld = S->bsz * H;
+    a.l = l, a.r = r, a.H = A, a.heads = S->heads, a.d = S->d, a.Lmax = S->L;
+    a.bs = S->bsz, a.ld = S->bsz * A;
     a.scale = 1.f / std::sqrt((float)S->d);
-    a.q = rowp(B.q, lr, H, e), a.kc = B.kc, a.vc = B.vc, a.o = rowp(B.o, lr, H, e), a.lse = B.lse;
+    a.q = rowp(B.q, lr, A, e), a.kc = B.kc, a.vc = B.vc, a.o = rowp(B.o, lr, A, e), a.lse = B.lse;
     a.dout = S->sc.dout, a.D = S->sc.D;
-    a.dq = rowp(B.dqkv, lr, 3 * H, e), a.ld_dq = (long)S->bsz * 3 * H, a.dq_seq = 3 * H;
+    a.dq = rowp(B.dqkv, lr, 3 * A, e), a.ld_dq = (long)S->bsz * 3 * A, a.dq_seq = 3 * A;
     a.dk = B.dk, a.dv = B.dv;
     const double pairs = ((double)ntok * l + (double)ntok * (ntok + 1) / 2) * S->bsz;
-    TRY(launch(S, K_ATTN_BWD, 8.0 * H * pairs,
-               ((4.0 * ntok + 2.0 * r) * H * e + 16.0 * r * H) * S->bsz,
+    TRY(launch(S, K_ATTN_BWD, 8.0 * A * pairs,
+               ((4.0 * ntok + 2.0 * r) * A * e + 16.0 * r * A) * S->bsz,
                [&] { return attn_bwd(dt, a, st); }));
-    TRY(launch(S, K_MISC, 0, 8.0 * n * H + 2 * nb, [&] {
-      return pack_dkv(dt, n, H, B.dk + (long)lr * H, B.dv + (long)lr * H,
-                      rowp(B.dqkv, lr, 3 * H, e), st);
+    TRY(launch(S, K_MISC, 0, (8.0 + 4.0 * e) * n * A, [&] {
+      return pack_dkv(dt, n, A, B.dk + (long)lr * A, B.dv + (long)lr * A,
+                      rowp(B.dqkv, lr, 3 * A, e), st);
     }));
     // QKV backward: du = [dq dk dv] W_qkv
-    g = nn(n, H, 3 * H, rowp(B.dqkv, lr, 3 * H, e), 3 * H, P.w_qkv);
+    g = nn(n, H, 3 * A, rowp(B.dqkv, lr, 3 * A, e), 3 * A, P.w_qkv);
     g.C = S->sc.du, g.ldc = H;
     TRY(run_gemm(S, K_GEMM_DX, g));
-    TRY(launch(S, K_MISC, 0, 3 * nb, [&] {
-      return colsum_acc(dt, n, 3 * H, rowp(B.dqkv, lr, 3 * H, e), 3 * H, (float*)G.b_qkv, st);
+    TRY(launch(S, K_MISC, 0, 3.0 * n * A * e, [&] {
+      return colsum_acc(dt, n, 3 * A, rowp(B.dqkv, lr, 3 * A, e), 3 * A, (float*)G.b_qkv, st);
     }));
     // LN1 backward + residual: dx = dx1 + LN1^T(du)
     void* out = li == 0 ? dx : rowp(S->lb[li - 1].dy, lr, H, e);
@@ -414,9 +420,10 @@ tp_status tp_stage_init(const tp_stage_config* cfg, const tp_layer_ptrs* params,
   if (!S) return TP_ERR_INVALID;
   S->cfg = *cfg;
   S->H = cfg->hidden;
-  S->F = 4 * cfg->hidden;
-  S->heads = cfg->heads;
+  S->heads = cfg->heads / parts_of(cfg);
   S->d = cfg->hidden / cfg->heads;
+  S->A = S->heads * S->d;
+  S->F = 4 * cfg->hidden / parts_of(cfg);
   S->L = cfg->max_seq;
   S->bsz = batch_of(cfg);
   S->dt = cfg->dtype == TP_DTYPE_FP32 ? DT_FP32 : DT_BF16;
@@ -441,7 +448,7 @@ void tp_stage_destroy(tp_stage* S) {
 
 tp_status tp_kv_prefix_reset(tp_stage* S) {
   if (!S) return TP_ERR_INVALID;
-  const size_t n = (size_t)S->L * S->bsz * S->H;
+  const size_t n = (size_t)S->L * S->bsz * S->A;
   for (auto& B : S->lb) {
     TRY(fill_f32(B.dk, n, 0.f, S->stream));
     TRY(fill_f32(B.dv, n, 0.f, S->stream));

@@ -38,7 +38,7 @@ EXPORTED = ("tp_stage_workspace_bytes", "tp_stage_init", "tp_stage_destroy",
 class StageConfig(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int), ("hidden", ctypes.c_int), ("heads", ctypes.c_int),
                 ("max_seq", ctypes.c_int), ("dtype", ctypes.c_int), ("wgrad_mode", ctypes.c_int),
-                ("ln_eps", ctypes.c_float), ("batch", ctypes.c_int)]
+                ("ln_eps", ctypes.c_float), ("batch", ctypes.c_int), ("op_parts", ctypes.c_int)]
 
 
 class LayerPtrs(ctypes.Structure):
@@ -120,10 +120,12 @@ def _check(status: int, what: str):
 
 
 def make_config(n_layers: int, hidden: int, heads: int, max_seq: int, dtype: str = "bf16",
-                wgrad: str = "per_slice", ln_eps: float = 1e-5, batch: int = 1) -> StageConfig:
+                wgrad: str = "per_slice", ln_eps: float = 1e-5, batch: int = 1,
+                op_parts: int = 1) -> StageConfig:
     return StageConfig(n_layers, hidden, heads, max_seq,
                        DTYPE_BF16 if dtype == "bf16" else DTYPE_FP32,
-                       WGRAD_PER_SLICE if wgrad == "per_slice" else WGRAD_DEFERRED, ln_eps, batch)
+                       WGRAD_PER_SLICE if wgrad == "per_slice" else WGRAD_DEFERRED, ln_eps, batch,
+                       op_parts)
 
 
 def workspace_bytes(cfg: StageConfig) -> int:
@@ -146,18 +148,22 @@ class Stage:
     [out, in].  Gradients are fp32 device tensors in ``self.grads`` (same keys),
     zero at construction.  The stage enqueues on the stream that is current at
     construction.  ``batch`` sequences move through the stage together (a batch
-    slice): slice tensors are then [n, batch, hidden] (token-major).
+    slice): slice tensors are then [n, batch, hidden] (token-major).  ``op_parts``
+    p > 1: the stage is one device's shard of p-way operation partitioning
+    (parameters of the shard's shapes, see ``synth.param_shapes``).
     """
 
     def __init__(self, params: List[Dict[str, torch.Tensor]], hidden: int, heads: int,
                  max_seq: int, dtype: str = "bf16", wgrad: str = "per_slice",
-                 ln_eps: float = 1e-5, device=None, batch: int = 1):
+                 ln_eps: float = 1e-5, device=None, batch: int = 1, op_parts: int = 1):
         self.n_layers = len(params)
         self.hidden, self.heads, self.max_seq, self.dtype = hidden, heads, max_seq, dtype
         self.batch = batch
         self.tdtype = torch_dtype(dtype)
         self.device = torch.device(device) if device is not None else params[0]["w_qkv"].device
-        self.cfg = make_config(self.n_layers, hidden, heads, max_seq, dtype, wgrad, ln_eps, batch)
+        self.op_parts = op_parts
+        self.cfg = make_config(self.n_layers, hidden, heads, max_seq, dtype, wgrad, ln_eps, batch,
+                               op_parts)
         for p in params:
             for k in SYNTH_NAMES:
                 t = p[k]

@@ -18,20 +18,21 @@ def rel_l2(a, b) -> float:
     return float(d / nb) if nb > 0 else float(d)
 
 
-def make_inputs(n_layers, H, L, dtype, seeds=(0, 1, 2), randomize_ln=False):
+def make_inputs(n_layers, H, L, dtype, seeds=(0, 1, 2), randomize_ln=False, op_parts=1):
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     sx, sp, sdy = seeds
-    params = synth.stage_params(n_layers, H, seed=sp, dtype=tdt, randomize_ln=randomize_ln)
+    params = synth.stage_params(n_layers, H, seed=sp, dtype=tdt, randomize_ln=randomize_ln,
+                                op_parts=op_parts)
     x = synth.hidden_states(L, H, seed=sx, dtype=tdt)
     dy = synth.upstream_grad(L, H, seed=sdy, dtype=tdt)
     return params, x, dy
 
 
 def run_gpu(params, x, dy, H, heads, L, dtype, fwd_lens, bwd_lens=None, wgrad="per_slice",
-            device="cuda:0"):
+            device="cuda:0", op_parts=1):
     from paper_2102_07988_amd import terapipe as tp
     dparams = [{k: v.to(device).contiguous() for k, v in p.items()} for p in params]
-    st = tp.Stage(dparams, H, heads, L, dtype=dtype, wgrad=wgrad)
+    st = tp.Stage(dparams, H, heads, L, dtype=dtype, wgrad=wgrad, op_parts=op_parts)
     y, dx = st.run_sequence(x.to(device), dy.to(device), fwd_lens, bwd_lens)
     torch.cuda.synchronize()
     out = {"y": y.float().cpu().numpy(), "dx": dx.float().cpu().numpy(),
@@ -40,29 +41,32 @@ def run_gpu(params, x, dy, H, heads, L, dtype, fwd_lens, bwd_lens=None, wgrad="p
     return out
 
 
-def run_oracle(params, x, dy, H, heads, L, fwd_lens, bwd_lens=None):
+def run_oracle(params, x, dy, H, heads, L, fwd_lens, bwd_lens=None, op_parts=1):
     from oracle import OracleStage
-    ost = OracleStage(synth.params_f64(params), H, heads, L)
+    ost = OracleStage(synth.params_f64(params), H, heads, L, op_parts=op_parts)
     y, dx = ost.run_sequence(synth.to_f64(x), synth.to_f64(dy), fwd_lens, bwd_lens)
     return {"y": y, "dx": dx, "grads": ost.grads}
 
 
-def make_batch_inputs(n_layers, H, L, batch, dtype, seeds=(0, 1, 2), randomize_ln=False):
+def make_batch_inputs(n_layers, H, L, batch, dtype, seeds=(0, 1, 2), randomize_ln=False,
+                      op_parts=1):
     """Parameters and [L, batch, H] inputs / upstream gradients."""
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     sx, sp, sdy = seeds
-    params = synth.stage_params(n_layers, H, seed=sp, dtype=tdt, randomize_ln=randomize_ln)
+    params = synth.stage_params(n_layers, H, seed=sp, dtype=tdt, randomize_ln=randomize_ln,
+                                op_parts=op_parts)
     x = synth.batch_hidden_states(L, batch, H, seed=sx, dtype=tdt)
     dy = synth.batch_upstream_grad(L, batch, H, seed=sdy, dtype=tdt)
     return params, x, dy
 
 
 def run_gpu_batch(params, x, dy, H, heads, L, dtype, fwd_lens, bwd_lens=None, wgrad="per_slice",
-                  device="cuda:0"):
+                  device="cuda:0", op_parts=1):
     """One batched stage (batch = x.shape[1]) over the whole sequence."""
     from paper_2102_07988_amd import terapipe as tp
     dparams = [{k: v.to(device).contiguous() for k, v in p.items()} for p in params]
-    st = tp.Stage(dparams, H, heads, L, dtype=dtype, wgrad=wgrad, batch=x.shape[1])
+    st = tp.Stage(dparams, H, heads, L, dtype=dtype, wgrad=wgrad, batch=x.shape[1],
+                  op_parts=op_parts)
     y, dx = st.run_sequence(x.to(device), dy.to(device), fwd_lens, bwd_lens)
     torch.cuda.synchronize()
     out = {"y": y.float().cpu().numpy(), "dx": dx.float().cpu().numpy(),
@@ -71,13 +75,13 @@ def run_gpu_batch(params, x, dy, H, heads, L, dtype, fwd_lens, bwd_lens=None, wg
     return out
 
 
-def run_oracle_batch(params, x, dy, H, heads, L, fwd_lens, bwd_lens=None):
+def run_oracle_batch(params, x, dy, H, heads, L, fwd_lens, bwd_lens=None, op_parts=1):
     """The sequences of a batch are independent: one oracle run per sequence,
     outputs stacked on axis 1, parameter gradients summed."""
     b = x.shape[1]
     ys, dxs, grads = [], [], None
     for s in range(b):
-        r = run_oracle(params, x[:, s], dy[:, s], H, heads, L, fwd_lens, bwd_lens)
+        r = run_oracle(params, x[:, s], dy[:, s], H, heads, L, fwd_lens, bwd_lens, op_parts)
         ys.append(r["y"])
         dxs.append(r["dx"])
         if grads is None:

@@ -94,6 +94,20 @@ def test_batch_config():
     tp.lib.tp_stage_destroy(h)
 
 
+def test_op_parts_config():
+    """Operation-partitioning shards: 0 means 1; heads and 4H must divide by p;
+    the arenas of the attention and FFN widths shrink with p."""
+    full = tp.workspace_bytes(tp.make_config(2, 64, 4, 32, "fp32", op_parts=1))
+    assert tp.workspace_bytes(tp.make_config(2, 64, 4, 32, "fp32", op_parts=0)) == full
+    half = tp.workspace_bytes(tp.make_config(2, 64, 4, 32, "fp32", op_parts=2))
+    assert 0 < half < full
+    assert tp.workspace_bytes(tp.make_config(2, 64, 4, 32, "fp32", op_parts=3)) == 0
+    assert tp.workspace_bytes(tp.make_config(2, 64, 4, 32, "fp32", op_parts=-1)) == 0
+    rc, h = _init(tp.make_config(2, 64, 4, 32, "fp32", op_parts=4))
+    assert rc == tp.TP_OK
+    tp.lib.tp_stage_destroy(h)
+
+
 def test_slice_order_errors_are_host_side():
     cfg = tp.make_config(1, 64, 4, 32, "fp32")
     rc, h = _init(cfg)
