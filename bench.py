@@ -24,16 +24,20 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-# name: (layers, hidden, heads, seq, default slicing)
+# name: (layers, hidden, heads, seq, default slicing, operation-partitioning shard p)
 WORKLOADS = {
-    "gpt3-175b-stage": (2, 12288, 96, 2048, [256] * 8),
-    "gpt3-175b-stage-8k": (2, 12288, 96, 8192, [512] * 16),
-    "gpt3-13b-stage": (2, 5120, 40, 2048, [256] * 8),
-    "gpt3-1.3b-stage": (2, 2048, 16, 2048, [256] * 8),
+    "gpt3-175b-stage": (2, 12288, 96, 2048, [256] * 8, 1),
+    "gpt3-175b-stage-8k": (2, 12288, 96, 8192, [512] * 16, 1),
+    "gpt3-13b-stage": (2, 5120, 40, 2048, [256] * 8, 1),
+    "gpt3-1.3b-stage": (2, 2048, 16, 2048, [256] * 8, 1),
+    # one GPU's work in the paper's 175B settings: (10) 48 stages of 2 layers,
+    # each layer split 8 ways; (9) 96 stages of 1 layer split 4 ways
+    "gpt3-175b-op8-stage": (2, 12288, 96, 2048, [256] * 8, 8),
+    "gpt3-175b-op4-stage": (1, 12288, 96, 2048, [256] * 8, 4),
 }
-# pipeline depth K of the paper's setting for each model (Table 1: settings (2), (4), (10))
+# pipeline depth K of the paper's setting for each model (Table 1: settings (2), (4), (10), (9))
 PAPER_K = {"gpt3-175b-stage": 48, "gpt3-175b-stage-8k": 48, "gpt3-13b-stage": 20,
-           "gpt3-1.3b-stage": 12}
+           "gpt3-1.3b-stage": 12, "gpt3-175b-op8-stage": 48, "gpt3-175b-op4-stage": 96}
 
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
@@ -74,7 +78,7 @@ def parse_slicing(s: str, L: int, default):
     return lens
 
 
-def cpu_baseline(params0, x, dy, hidden: int, heads: int, n_tokens: int):
+def cpu_baseline(params0, x, dy, hidden: int, heads: int, n_tokens: int, op_parts: int = 1):
     """Time the fp64 oracle (all host threads) on one layer of the workload
     (the benchmark's own layer-0 parameters) over one slice of the first
     n_tokens tokens after no context: forward + backward."""
@@ -86,17 +90,18 @@ def cpu_baseline(params0, x, dy, hidden: int, heads: int, n_tokens: int):
     p64 = {k: v.detach().to("cpu").to(torch.float64).numpy() for k, v in params0.items()}
     x64 = x[:n_tokens].to("cpu").to(torch.float64).numpy()
     dy64 = dy[:n_tokens].to("cpu").to(torch.float64).numpy()
-    st = OracleStage([p64], hidden, heads, n_tokens)
+    st = OracleStage([p64], hidden, heads, n_tokens, op_parts=op_parts)
     del p64
     t0 = time.perf_counter()
     st.run_sequence(x64, dy64, [n_tokens])
     dt = time.perf_counter() - t0
-    flops = slice_flops(n_tokens, 0, hidden)
+    flops = slice_flops(n_tokens, 0, hidden) // op_parts
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "seconds": round(dt, 3),
-            "sample": f"1 layer of the same shape (H={hidden}, {heads} heads), one slice of "
-                      f"{n_tokens} tokens at context 0, forward+backward, fp64"}
+            "sample": f"1 layer of the same shape (H={hidden}, {heads // op_parts} of {heads} "
+                      f"heads), one slice of {n_tokens} tokens at context 0, forward+backward, "
+                      f"fp64"}
 
 
 def _subset(U: int):
@@ -132,7 +137,7 @@ def _slicing_summary(tp, cost, unit, K):
 
 def pipeline_report(st, tp, L: int, unit: int, K: int, warmup: int, reps: int,
                     run_slicing, dw_ms: float, fine_unit: int, n_layers: int, H: int,
-                    deferred: bool, fine_K=(48, 96)):
+                    deferred: bool, fine_K=(48, 96), op_parts: int = 1):
     """Per-slice cost tables t(len, ctx) = t_fwd + t_bwd of this stage and the
     slicings they give for a pipeline of K such stages (Eq. 5-8, Algorithm 1):
 
@@ -166,6 +171,7 @@ def pipeline_report(st, tp, L: int, unit: int, K: int, warmup: int, reps: int,
                 continue
             t_ns = int(cost[n // unit - 1, c // unit])
             fl = n_layers * (tp.slice_flops(n, c, H) - (24 * n * H * H if deferred else 0))
+            fl //= op_parts
             pts.append({"len": n, "ctx": c, "t_ms": round(t_ns / 1e6, 3),
                         "tflops": round(fl / (t_ns * 1e-9) / 1e12, 1),
                         "pct_bf16_peak": round(100 * fl / (t_ns * 1e-9) / 1e12 / PEAK_BF16_TFLOPS, 1)})
@@ -313,7 +319,7 @@ def main():
     from paper_2102_07988_amd import synth
     from paper_2102_07988_amd import terapipe as tp
 
-    n_layers, H, heads, L, default_sl = WORKLOADS[args.workload]
+    n_layers, H, heads, L, default_sl, parts = WORKLOADS[args.workload]
     dp_source = None
     lens = parse_slicing(args.slicing, L, default_sl) if args.slicing != "dp" else None
     dev = torch.device("cuda:0")
@@ -322,10 +328,11 @@ def main():
     cs = torch.cuda.Stream(device=dev)
     torch.cuda.set_stream(cs)
     bf = torch.bfloat16
-    params = synth.stage_params(n_layers, H, seed=synth.SEED_PARAMS, dtype=bf, device=dev)
+    params = synth.stage_params(n_layers, H, seed=synth.SEED_PARAMS, dtype=bf, device=dev,
+                                op_parts=parts)
     x = synth.hidden_states(L, H, seed=synth.SEED_X, dtype=bf, device=dev)
     dy = synth.upstream_grad(L, H, seed=synth.SEED_DY, dtype=bf, device=dev)
-    st = tp.Stage(params, H, heads, L, dtype="bf16", wgrad=args.wgrad)
+    st = tp.Stage(params, H, heads, L, dtype="bf16", wgrad=args.wgrad, op_parts=parts)
     if lens is None:
         # slicing chosen by the DP (Eq. 5-8, Algorithm 1) on this stage's own
         # model-mode cost table (Eq. 9) at the paper's pipeline depth for the model
@@ -398,7 +405,7 @@ def main():
     flops_step = 0
     c = 0
     for n in lens:
-        flops_step += tp.slice_flops(n, c, H) * n_layers
+        flops_step += tp.slice_flops(n, c, H) * n_layers // parts
         c += n
     ms = (t1 - t0) * 1e3 / args.steps
     value = flops_step / (ms * 1e-3) / 1e12
@@ -443,7 +450,9 @@ def main():
         "config": {"workload": args.workload, "layers": n_layers, "hidden": H, "heads": heads,
                    "seq_len": L, "batch": 1, "slicing": lens, "wgrad": args.wgrad,
                    **({"slicing_source": dp_source} if dp_source else {}),
-                   "global_batch": 1, "parallelism": "one pipeline stage"},
+                   "global_batch": 1,
+                   "parallelism": "one pipeline stage" if parts == 1 else
+                   f"one pipeline stage, shard of {parts}-way operation partitioning"},
         "pct_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "flops_per_step": flops_step, "outputs_finite": finite,
         "roofline": roofline, "kernels": kernels,
@@ -474,18 +483,20 @@ def main():
 
         rep = pipeline_report(st, tp, L, args.pipeline_unit, args.pipeline_K, 1, 3,
                               run_slicing, dw_ms, args.pipeline_fine_unit, n_layers, H,
-                              args.wgrad == "deferred")
+                              args.wgrad == "deferred", op_parts=parts)
         fine_cost = rep.pop("_fine_cost", None)
         if args.joint_batch >= 2 and fine_cost is not None:
             rep["joint"] = joint_report(
-                lambda b: tp.Stage(params, H, heads, L, dtype="bf16", wgrad=args.wgrad, batch=b),
+                lambda b: tp.Stage(params, H, heads, L, dtype="bf16", wgrad=args.wgrad, batch=b,
+                                   op_parts=parts),
                 tp, L, args.pipeline_fine_unit, PAPER_K[args.workload], args.joint_batch,
                 fine_cost, 1, 3)
         out["pipeline"] = rep
         st.zero_grads()
     out["mfma_probe_tflops"] = round(tp.measure_mfma_peak(), 1)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(params[0], x, dy, H, heads, args.cpu_baseline_tokens)
+        out["cpu_baseline"] = cpu_baseline(params[0], x, dy, H, heads, args.cpu_baseline_tokens,
+                                           parts)
     print(json.dumps(out), flush=True)
 
 
