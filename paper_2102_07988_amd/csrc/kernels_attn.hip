@@ -169,9 +169,12 @@ struct Tile {
 
 // two waves per SIMD (registers capped at 256): one wave's softmax overlaps the
 // other's matrix products
-template <int D, int NW>
+// SPLIT: this block takes only split blockIdx.z % nsplit of the keys and
+// leaves the unnormalised output with its running maximum and sum.
+template <int D, int NW, bool SPLIT>
 __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a0) {
   const AttnArgs a = attn_seq_view<uint16_t>(a0);
+  const int zsp = SPLIT ? blockIdx.z % a.nsplit : 0;
   using T = Tile<D>;
   constexpr int NTH = 64 * NW, BKV = 64, KS = D / 16, JB = D / 32, ST = 2;
   constexpr int TILE = BKV * D, STAGE = 2 * TILE;       // elements: K then V
@@ -207,7 +210,11 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a0) {
 #pragma unroll
   for (int j = 0; j < JB; ++j) o[j] = zero16();
 
-  const int nkb = (kend_blk + BKV - 1) / BKV;
+  int nkb = (kend_blk + BKV - 1) / BKV, kb0 = 0;
+  if constexpr (SPLIT) {
+    kb0 = zsp * (a.kv_chunk / BKV);
+    nkb = min(nkb, kb0 + a.kv_chunk / BKV);
+  }
   const typename T::template Dma<BKV, NTH> kvd(H, __builtin_amdgcn_readfirstlane(w));
   auto issue = [&](int stage, int kb) {
     uint16_t* st = smem + stage * STAGE;
@@ -215,8 +222,8 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a0) {
     kvd.issue(Kc + (long)kb * BKV * H, H, rv, st);
     kvd.issue(Vc + (long)kb * BKV * H, H, rv, st + TILE);
   };
-  issue(0, 0);
-  for (int kb = 0; kb < nkb; ++kb) {
+  if (kb0 < nkb) issue(kb0 % ST, kb0);
+  for (int kb = kb0; kb < nkb; ++kb) {
     wait_vm<0>();
     __builtin_amdgcn_s_barrier();
     if (kb + 1 < nkb) issue((kb + 1) % ST, kb + 1);
@@ -298,7 +305,23 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a0) {
       }
     }
   }
-  if (tvalid) {
+  if (SPLIT && tvalid) {
+    // partial of split zsp: rows like o (stride H = ld), one [rows][a.H] plane per split
+    const int n = a.r - a.l, s = blockIdx.z / a.nsplit;
+    float* P = a.ws + (long)zsp * n * a.bs * a.H + (long)s * a.H + (long)(t - a.l) * H + h * D;
+#pragma unroll
+    for (int j = 0; j < JB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; v += 4)
+        *(float4*)(P + 32 * j + 8 * (v >> 2) + 4 * G) =
+            make_float4(o[j][v], o[j][v + 1], o[j][v + 2], o[j][v + 3]);
+    if (G == 0) {
+      float* ml = a.ws + (long)a.nsplit * n * a.bs * a.H +
+                  ((((long)zsp * a.bs + s) * a.heads + h) * n + (t - a.l)) * 2;
+      ml[0] = m;
+      ml[1] = lsum;
+    }
+  } else if (tvalid) {
     const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
     uint16_t* O = (uint16_t*)a.o + (long)(t - a.l) * H + h * D;
 #pragma unroll
@@ -573,9 +596,12 @@ __global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma
 
 // ------------------------------------------------------------------- dQ
 
-template <int D, int NW>
+// SPLIT: this block takes only split blockIdx.z % nsplit of the keys and
+// leaves its unscaled fp32 dQ partial.
+template <int D, int NW, bool SPLIT>
 __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a0) {
   const AttnArgs a = attn_seq_view<uint16_t>(a0);
+  const int zsp = SPLIT ? blockIdx.z % a.nsplit : 0;
   using T = Tile<D>;
   constexpr int NTH = 64 * NW, BKV = 64, KS = D / 16, JB = D / 32, ST = 2;
   constexpr int TILE = BKV * D, STAGE = 2 * TILE;  // K then V
@@ -608,7 +634,11 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a0) {
 #pragma unroll
   for (int j = 0; j < JB; ++j) dq[j] = zero16();
 
-  const int nkb = (kend_blk + BKV - 1) / BKV;
+  int nkb = (kend_blk + BKV - 1) / BKV, kb0 = 0;
+  if constexpr (SPLIT) {
+    kb0 = zsp * (a.kv_chunk / BKV);
+    nkb = min(nkb, kb0 + a.kv_chunk / BKV);
+  }
   const typename T::template Dma<BKV, NTH> kvd(H, __builtin_amdgcn_readfirstlane(w));
   auto issue = [&](int stage, int kb) {
     uint16_t* st = smem + stage * STAGE;
@@ -616,8 +646,8 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a0) {
     kvd.issue(Kc + (long)kb * BKV * H, H, rv, st);
     kvd.issue(Vc + (long)kb * BKV * H, H, rv, st + TILE);
   };
-  issue(0, 0);
-  for (int kb = 0; kb < nkb; ++kb) {
+  if (kb0 < nkb) issue(kb0 % ST, kb0);
+  for (int kb = kb0; kb < nkb; ++kb) {
     wait_vm<0>();
     __builtin_amdgcn_s_barrier();
     if (kb + 1 < nkb) issue((kb + 1) % ST, kb + 1);
@@ -679,7 +709,16 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a0) {
       }
     }
   }
-  if (tvalid) {
+  if (SPLIT && tvalid) {
+    const int n = a.r - a.l, s = blockIdx.z / a.nsplit;
+    float* P = a.ws + (long)zsp * n * a.bs * a.H + (long)s * a.H + (long)(t - a.l) * H + h * D;
+#pragma unroll
+    for (int j = 0; j < JB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; v += 4)
+        *(float4*)(P + 32 * j + 8 * (v >> 2) + 4 * G) =
+            make_float4(dq[j][v], dq[j][v + 1], dq[j][v + 2], dq[j][v + 3]);
+  } else if (tvalid) {
     uint16_t* dQ = (uint16_t*)a.dq + (long)(t - a.l) * a.ld_dq + h * D;
 #pragma unroll
     for (int j = 0; j < JB; ++j)
@@ -693,7 +732,85 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a0) {
   }
 }
 
+// ------------------------------------------------------ split combines
+
+// Forward: one wave per (row, head) merges the splits' partials in split
+// order: M = max_z m_z, L = sum_z l_z 2^(m_z - M), O = sum_z O_z 2^(m_z - M) / L.
+template <int D>
+__global__ __launch_bounds__(256) void attn_fwd_combine(AttnArgs a) {
+  const int n = a.r - a.l, lane = threadIdx.x & 63;
+  const long rows = (long)n * a.bs, wave = ((long)blockIdx.x * 256 + threadIdx.x) >> 6;
+  if (wave >= rows * a.heads) return;
+  const int i = (int)(wave / a.heads), h = (int)(wave % a.heads);  // row i = (t - l) bs + s
+  const int tl = i / a.bs, s = i % a.bs;
+  const long plane = rows * a.H;
+  const float* part = a.ws + (long)i * a.H + h * D;
+  const float* ml = a.ws + a.nsplit * plane + (((long)s * a.heads + h) * n + tl) * 2;
+  const long ml_split = (long)a.bs * a.heads * n * 2;
+  float M = -INFINITY;
+  for (int z = 0; z < a.nsplit; ++z) M = fmaxf(M, ml[z * ml_split]);
+  // weight of split z (0 for a split that saw no key of this query)
+  auto fz = [&](int z) {
+    const float mz = ml[z * ml_split];
+    return mz == -INFINITY ? 0.f : exp2_fast(mz - M);
+  };
+  float L = 0.f;
+  for (int z = 0; z < a.nsplit; ++z) L += ml[z * ml_split + 1] * fz(z);
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+  uint16_t* O = (uint16_t*)a.o + (long)i * a.H + h * D;
+  for (int j = lane; j < D; j += 64) {
+    float acc = 0.f;
+    for (int z = 0; z < a.nsplit; ++z) acc += part[z * plane + j] * fz(z);
+    O[j] = f32_to_bf16_bits(acc * inv);
+  }
+  if (lane == 0) a.lse[((long)s * a.heads + h) * a.Lmax + a.l + tl] = (M + log2f(L)) * LN2;
+}
+
+// dQ: the splits' partials added in split order, scaled, stored as bf16 rows.
+__global__ __launch_bounds__(256) void attn_dq_combine(AttnArgs a) {
+  const int n = a.r - a.l;
+  const long rows = (long)n * a.bs, a8 = a.H / 8;
+  const long e = (long)blockIdx.x * 256 + threadIdx.x;
+  if (e >= rows * a8) return;
+  const long i = e / a8, col = (e - i * a8) * 8;
+  const long plane = rows * a.H;
+  float acc[8] = {};
+  for (int z = 0; z < a.nsplit; ++z) {
+    const float4* p = (const float4*)(a.ws + z * plane + i * a.H + col);
+    const float4 u = p[0], w = p[1];
+    acc[0] += u.x, acc[1] += u.y, acc[2] += u.z, acc[3] += u.w;
+    acc[4] += w.x, acc[5] += w.y, acc[6] += w.z, acc[7] += w.w;
+  }
+  uint16_t* dst = (uint16_t*)a.dq + (i / a.bs) * a.ld_dq + (i % a.bs) * a.dq_seq + col;
+  uint4 o;
+  o.x = pack_bf16x2(acc[0] * a.scale, acc[1] * a.scale);
+  o.y = pack_bf16x2(acc[2] * a.scale, acc[3] * a.scale);
+  o.z = pack_bf16x2(acc[4] * a.scale, acc[5] * a.scale);
+  o.w = pack_bf16x2(acc[6] * a.scale, acc[7] * a.scale);
+  *(uint4*)dst = o;
+}
+
 constexpr int NWF = 4;  // waves per block
+constexpr int MAX_SPLIT = 8;
+
+// Key-range splits for a query-parallel launch that fills under half of the
+// 256 CUs: enough splits for about one block per CU, at most MAX_SPLIT, each
+// of at least one 64-key block, within the scratch (measured: a launch of 192
+// blocks is faster unsplit -- the partials' traffic outweighs the extra
+// blocks).  Sets a.nsplit and a.kv_chunk; 1 = no split.
+void plan_split(AttnArgs& a, bool with_ml) {
+  a.nsplit = 1;
+  const int n = a.r - a.l;
+  const long wgs = (long)cdiv(n, 32 * NWF) * a.heads * a.bs;
+  if (!a.ws || wgs >= 128) return;
+  int ns = (int)std::min<long>(MAX_SPLIT, cdiv(256, wgs));
+  ns = std::min(ns, cdiv(a.r, 64));
+  const long per = (long)n * a.bs * a.H + (with_ml ? 2L * a.bs * a.heads * n : 0);
+  while (ns > 1 && ns * per > a.ws_elems) --ns;
+  if (ns < 2) return;
+  a.kv_chunk = cdiv(cdiv(a.r, ns), 64) * 64;
+  a.nsplit = cdiv(a.r, a.kv_chunk);
+}
 // dK/dV as one kernel (0) or as a dV kernel (1) followed by a dK kernel (2)
 #ifndef TP_DKDV_MODE_A
 #define TP_DKDV_MODE_A 1
@@ -711,9 +828,21 @@ template <int D>
 hipError_t fwd_d(const AttnArgs& a, hipStream_t s) {
   const int n = a.r - a.l;
   constexpr size_t lds = 2 * 2 * 64 * D * 2;
-  hipError_t e = set_lds(attn_fwd_mfma<D, NWF>, lds);
+  AttnArgs b = a;
+  plan_split(b, true);
+  if (b.nsplit == 1) {
+    hipError_t e = set_lds(attn_fwd_mfma<D, NWF, false>, lds);
+    if (e != hipSuccess) return e;
+    attn_fwd_mfma<D, NWF, false><<<dim3(cdiv(n, 32 * NWF), a.heads, a.bs), 64 * NWF, lds, s>>>(a);
+    return hipGetLastError();
+  }
+  hipError_t e = set_lds(attn_fwd_mfma<D, NWF, true>, lds);
   if (e != hipSuccess) return e;
-  attn_fwd_mfma<D, NWF><<<dim3(cdiv(n, 32 * NWF), a.heads, a.bs), 64 * NWF, lds, s>>>(a);
+  attn_fwd_mfma<D, NWF, true>
+      <<<dim3(cdiv(n, 32 * NWF), a.heads, a.bs * b.nsplit), 64 * NWF, lds, s>>>(b);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  attn_fwd_combine<D><<<cdiv((long)n * a.bs * a.heads, 4), 256, 0, s>>>(b);
   return hipGetLastError();
 }
 
@@ -746,9 +875,22 @@ hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
   }
   constexpr size_t lds_q = 2 * 2 * 64 * D * 2;
-  e = set_lds(attn_bwd_dq_mfma<D, NWF>, lds_q);
+  AttnArgs b = a;
+  plan_split(b, false);
+  if (b.nsplit == 1) {
+    e = set_lds(attn_bwd_dq_mfma<D, NWF, false>, lds_q);
+    if (e != hipSuccess) return e;
+    attn_bwd_dq_mfma<D, NWF, false>
+        <<<dim3(cdiv(n, 32 * NWF), a.heads, a.bs), 64 * NWF, lds_q, s>>>(a);
+    return hipGetLastError();
+  }
+  e = set_lds(attn_bwd_dq_mfma<D, NWF, true>, lds_q);
   if (e != hipSuccess) return e;
-  attn_bwd_dq_mfma<D, NWF><<<dim3(cdiv(n, 32 * NWF), a.heads, a.bs), 64 * NWF, lds_q, s>>>(a);
+  attn_bwd_dq_mfma<D, NWF, true>
+      <<<dim3(cdiv(n, 32 * NWF), a.heads, a.bs * b.nsplit), 64 * NWF, lds_q, s>>>(b);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  attn_dq_combine<<<cdiv((long)n * a.bs * (a.H / 8), 256), 256, 0, s>>>(b);
   return hipGetLastError();
 }
 

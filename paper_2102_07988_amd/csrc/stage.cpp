@@ -34,6 +34,8 @@ struct Scratch {
   void *io_a, *io_b;      // profiler slice buffers [Lmax][H]
   float* splitk;          // split-K partial sums of the slice GEMMs
   size_t splitk_elems;
+  float* attn;            // key-split partials of the query-parallel attention kernels
+  size_t attn_elems;
 };
 
 struct Carver {
@@ -150,6 +152,14 @@ size_t carve(const tp_stage_config* c, void* base, std::vector<LayerBufs>* lbs, 
   // up to 8 partial [min(L, 256)][widest product output] fp32 products
   s.splitk_elems = 8 * std::min<size_t>(L, 256) * std::max(std::max(F, H), 3 * A);
   s.splitk = (float*)cv.take(s.splitk_elems * 4);
+  // attention key splits happen for launches of under 128 blocks of 128 queries
+  // (fewer than 16384 query-heads): at most 8 splits of [rows][A] partials and
+  // per-query (max, sum) pairs
+  {
+    const size_t d = H / c->heads, qh = std::min<size_t>(L * a, 16384);
+    s.attn_elems = 8 * (qh * d + 2 * qh);
+    s.attn = (float*)cv.take(s.attn_elems * 4);
+  }
   if (sc) *sc = s;
   return (cv.off + 255) & ~(size_t)255;
 }
@@ -273,6 +283,7 @@ tp_status forward_impl(tp_stage* S, int l, int r, const void* x, void* y) {
     AttnArgs a;
     a.l = l, a.r = r, a.H = A, a.heads = S->heads, a.d = S->d, a.Lmax = S->L;
     a.bs = S->bsz, a.ld = S->bsz * A;
+    a.ws = S->sc.attn, a.ws_elems = (long)S->sc.attn_elems;
     a.scale = 1.f / std::sqrt((float)S->d);
     a.q = rowp(B.q, lr, A, e), a.kc = B.kc, a.vc = B.vc, a.o = rowp(B.o, lr, A, e), a.lse = B.lse;
     const double pairs = ((double)ntok * l + (double)ntok * (ntok + 1) / 2) * S->bsz;
@@ -344,6 +355,7 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
     AttnArgs a;
     a.l = l, a.r = r, a.H = A, a.heads = S->heads, a.d = S->d, a.Lmax = S->L;
     a.bs = S->bsz, a.ld = S->bsz * A;
+    a.ws = S->sc.attn, a.ws_elems = (long)S->sc.attn_elems;
     a.scale = 1.f / std::sqrt((float)S->d);
     a.q = rowp(B.q, lr, A, e), a.kc = B.kc, a.vc = B.vc, a.o = rowp(B.o, lr, A, e), a.lse = B.lse;
     a.dout = S->sc.dout, a.D = S->sc.D;

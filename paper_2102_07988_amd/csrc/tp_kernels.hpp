@@ -78,13 +78,22 @@ struct AttnArgs {
   long ld_dq = 0, dq_seq = 0;
   float* dk = nullptr;  // fp32 accumulation buffers (absolute rows)
   float* dv = nullptr;
+  // Key-range split of the query-parallel kernels (forward, dQ) when their
+  // grid is small: blockIdx.z = sequence * nsplit + split, split z takes keys
+  // [z * kv_chunk, (z + 1) * kv_chunk), and writes fp32 partials that a
+  // combine kernel adds up in split order.  part: [nsplit][(r-l) * bs][H]
+  // (rows as in q); ml (forward): [nsplit][bs][heads][r-l] pairs of (running
+  // maximum in log2 units, sum of weights).  Scratch of ws_elems floats.
+  int nsplit = 1, kv_chunk = 0;
+  float* ws = nullptr;
+  long ws_elems = 0;
 };
 // The arguments of sequence blockIdx.z of the batch as a one-sequence view:
 // pointers moved to its columns (element type T) and planes; the row stride
 // stays a.ld.
 template <typename T>
 __device__ inline AttnArgs attn_seq_view(AttnArgs a) {
-  const int s = blockIdx.z;
+  const int s = blockIdx.z / a.nsplit;
   if (s == 0) return a;
   const long off = (long)s * a.H, plane = (long)s * a.heads * a.Lmax;
   a.q = (const T*)a.q + off;
