@@ -847,6 +847,9 @@ hipError_t fwd_d(const AttnArgs& a, hipStream_t s) {
 }
 
 template <int D>
+hipError_t dq_d(const AttnArgs& a, hipStream_t s);
+
+template <int D>
 hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
   const int n = a.r - a.l;
   attn_bwd_rowdot<D><<<dim3(cdiv((long)n * a.heads, 4), 1, a.bs), 256, 0, s>>>(a);
@@ -860,6 +863,23 @@ hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
   constexpr int NWK = D == 128 ? 8 : 4, STK = D == 128 ? 4 : 2;
   constexpr size_t lds_a = STA * (2 * 32 * D + NWF * 128) * 2;
   constexpr size_t lds_k = STK * (2 * 32 * D + NWK * 128) * 2 + 32 * NWK * D * 2;
+  if (DKDV_MODE_A != 0 && (long)cdiv(a.r, 32 * NWF) * a.heads * a.bs < 128) {
+    // few key blocks (few heads, short prefix): two-wave dV blocks and
+    // four-wave dK blocks over two-tile rings, so more blocks share the CUs
+    constexpr size_t lds_v2 = 2 * (2 * 32 * D + 2 * 128) * 2;
+    constexpr size_t lds_k4 = 2 * (2 * 32 * D + 4 * 128) * 2 + 32 * 4 * D * 2;
+    e = set_lds(attn_bwd_dkdv_mfma<D, 2, 1, 2>, lds_v2);
+    if (e != hipSuccess) return e;
+    attn_bwd_dkdv_mfma<D, 2, 1, 2><<<dim3(cdiv(a.r, 64), a.heads, a.bs), 128, lds_v2, s>>>(a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = set_lds(attn_bwd_dkdv_mfma<D, 4, 2, 2>, lds_k4);
+    if (e != hipSuccess) return e;
+    attn_bwd_dkdv_mfma<D, 4, 2, 2><<<dim3(cdiv(a.r, 128), a.heads, a.bs), 256, lds_k4, s>>>(a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return dq_d<D>(a, s);
+  }
   e = set_lds(attn_bwd_dkdv_mfma<D, NWF, DKDV_MODE_A, STA>, lds_a);
   if (e != hipSuccess) return e;
   attn_bwd_dkdv_mfma<D, NWF, DKDV_MODE_A, STA>
@@ -874,6 +894,13 @@ hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  return dq_d<D>(a, s);
+}
+
+template <int D>
+hipError_t dq_d(const AttnArgs& a, hipStream_t s) {
+  const int n = a.r - a.l;
+  hipError_t e;
   constexpr size_t lds_q = 2 * 2 * 64 * D * 2;
   AttnArgs b = a;
   plan_split(b, false);
