@@ -550,17 +550,21 @@ hipError_t launch_dma(const GemmArgs& a, hipStream_t s) {
 
 // One DMA GEMM launch.  Every configuration holds one workgroup per CU (its
 // LDS ring takes most of the 160 KB), so when the tile count is low the
-// reduction is split (<= 8 splits of >= 8 k-tiles; whole k-tiles, the last
-// split may be shorter) by the cost model below.
+// reduction is split (whole k-tiles, the last split may be shorter).
+// force_splits > 0 takes that many splits (at most; as k-tiles allow),
+// otherwise the split count comes from the cost model below (<= 8 splits of
+// >= 8 k-tiles).
 template <int BM, int BN, int BK, int WGM, int WGN, bool A_KC, bool B_KC, int STAGES,
           int SB = STAGES>
-hipError_t run_dma(GemmArgs a, hipStream_t s) {
+hipError_t run_dma(GemmArgs a, hipStream_t s, int force_splits = 0) {
   constexpr int CUS = 256;
   if (a.K % BK) return hipErrorNotSupported;
   const long tiles = (long)cdiv(a.M, BM) * cdiv(a.N, BN);
   const int nkt = a.K / BK;
   int splits = 1;
-  if (a.ws && tiles < 2 * CUS) {
+  if (force_splits > 0) {
+    splits = a.ws && (long)force_splits * a.M * a.N <= a.ws_elems ? std::min(force_splits, nkt) : 1;
+  } else if (a.ws && tiles < 2 * CUS) {
     // time ~ rounds(s) / s of the unsplit main loop, plus the partial-sum
     // traffic (s fp32 products written and read back), which relative to the
     // weight stream of one round is about 2.2 M / K per split
@@ -589,14 +593,57 @@ hipError_t run_dma(GemmArgs a, hipStream_t s) {
 }
 
 template <bool A_KC, bool B_KC>
-hipError_t run_cfg_id(int cfg, const GemmArgs& a, hipStream_t s) {
+hipError_t run_cfg_id(int cfg, const GemmArgs& a, hipStream_t s, int splits = 0) {
   switch (cfg) {
-    case 0: return run_dma<128, 128, 64, 2, 2, A_KC, B_KC, 4>(a, s);
-    case 1: return run_dma<256, 128, 64, 4, 2, A_KC, B_KC, 3>(a, s);
-    case 2: return run_dma<256, 256, 64, 2, 4, A_KC, B_KC, 2>(a, s);
-    case 3: return run_dma<256, 256, 64, 2, 4, A_KC, B_KC, 2, 3>(a, s);
+    case 0: return run_dma<128, 128, 64, 2, 2, A_KC, B_KC, 4>(a, s, splits);
+    case 1: return run_dma<256, 128, 64, 4, 2, A_KC, B_KC, 3>(a, s, splits);
+    case 2: return run_dma<256, 256, 64, 2, 4, A_KC, B_KC, 2>(a, s, splits);
+    case 3: return run_dma<256, 256, 64, 2, 4, A_KC, B_KC, 2, 3>(a, s, splits);
     default: return hipErrorNotSupported;
   }
+}
+
+// Tile shape and split count for a product whose A operand is k-contiguous
+// (slice activations or output gradients times a weight matrix): the
+// candidate (tiles, splits) with the smallest modelled time.  The model was
+// fitted (log least squares, rms error 9 %) to a sweep of every candidate on
+// the stage's products for hidden sizes 2048-12288, operation-partitioning
+// shards and 128-512 rows:
+//   t = max(rounds * (0.68 + kt * c_kt), rows_tiles * N * K * 2 B * 0.178 us/MB)
+//       + (splits > 1 ? 5.5 + splits * M * N * 8 B / 5.8 MB/us : 0)
+// with rounds = workgroups / 256 rounded up, kt = k-tiles per split and c_kt
+// = 0.62 / 0.98 / 1.60 us for 128x128 / 256x128 / 256x256 tiles: a round of
+// workgroups, not below the weight stream from HBM, plus the partial sums.
+struct TileChoice {
+  int cfg, splits;
+};
+TileChoice choose_tiles(const GemmArgs& a) {
+  static const int kSplits[] = {1, 2, 3, 4, 5, 6, 8, 10, 12, 16};
+  struct Cand {
+    int cfg, bm, bn;
+    double c_kt;
+  };
+  static const Cand kCands[] = {{0, 128, 128, 0.6208}, {1, 256, 128, 0.9844}, {3, 256, 256, 1.601}};
+  const int nkt = a.K / 64;
+  double best = 1e300;
+  TileChoice pick{3, 1};
+  for (const Cand& c : kCands) {
+    const long mt = cdiv(a.M, c.bm), tiles = mt * cdiv(a.N, c.bn);
+    const double hbm = (double)mt * a.N * a.K * 2.0 / 1e6 * 0.1783;
+    for (int sp : kSplits) {
+      if (sp > nkt) break;
+      if (sp > 1 && (!a.ws || (long)sp * a.M * a.N > a.ws_elems)) break;
+      const int ks = cdiv(nkt, sp), s = cdiv(nkt, ks);
+      const long rounds = cdiv(tiles * s, 256);
+      double t = std::max(rounds * (0.6789 + ks * c.c_kt), hbm);
+      if (s > 1) t += 5.5466 + (double)s * a.M * a.N * 8.0 / 1e6 / 5.7959;
+      if (t < best) {
+        best = t;
+        pick = {c.cfg, s};
+      }
+    }
+  }
+  return pick;
 }
 
 }  // namespace
@@ -618,18 +665,22 @@ hipError_t gemm_dma_bf16_cfg(int cfg, const GemmArgs& a, hipStream_t s) {
   // operands) as 8-column segments
   if (a.epi == EPI_ACC_F32 && (((uintptr_t)a.C & 15) || (a.ldc & 3))) return hipErrorNotSupported;
   if (a.epi != EPI_ACC_F32 && !vec8_ok(a)) return hipErrorNotSupported;
+  int splits = 0;
   if (cfg < 0) {
-    // measured on the stage shapes: 256 x 256 tiles everywhere except small row
-    // counts and wide forward outputs of slices, which prefer 256 x 128 (3
-    // stages); products with the weights as B (activations or output gradients
-    // as A, k-contiguous) keep the weight stream a k-tile further ahead
-    if (a_mc && b_nc) cfg = 2;
-    else if (a.M <= 128) cfg = 0;
-    else if (a_kc && b_kc && a.M <= 256 && a.N >= 4 * a.K) cfg = 1;
-    else cfg = 3;
+    // weight-gradient products (both operands m/n-contiguous): 256 x 256 tiles
+    // over one (A, B) ring; products with a weight matrix as B: the modelled
+    // best tile shape and split count (256 x 256 tiles keep the weight stream
+    // a k-tile further ahead than the activations)
+    if (a_mc && b_nc) {
+      cfg = 2;
+    } else {
+      const TileChoice c = choose_tiles(a);
+      cfg = c.cfg;
+      splits = c.splits;
+    }
   }
-  if (a_kc && b_kc) return run_cfg_id<true, true>(cfg, a, s);
-  if (a_kc && b_nc) return run_cfg_id<true, false>(cfg, a, s);
+  if (a_kc && b_kc) return run_cfg_id<true, true>(cfg, a, s, splits);
+  if (a_kc && b_nc) return run_cfg_id<true, false>(cfg, a, s, splits);
   if (a_mc && b_nc) {
     if (a.M < 128 || a.N < 128) return hipErrorNotSupported;
     return run_cfg_id<false, false>(cfg, a, s);
