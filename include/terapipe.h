@@ -60,7 +60,8 @@ typedef enum { TP_DTYPE_BF16 = 0, TP_DTYPE_FP32 = 1 } tp_dtype;
  * weight-gradient GEMMs run once over the whole sequence (reduction length =
  * number of cached tokens) when the backward frontier reaches position 0.
  * Both give the same gradients up to fp32 summation order.  Bias and
- * LayerNorm-parameter gradients are accumulated per slice in both modes. */
+ * LayerNorm-parameter gradients (column sums over tokens) follow the same
+ * mode: per slice, or once per sequence from kept per-token gradients. */
 typedef enum { TP_WGRAD_PER_SLICE = 0, TP_WGRAD_DEFERRED = 1 } tp_wgrad_mode;
 
 typedef struct {
@@ -146,7 +147,8 @@ tp_status tp_slice_backward(tp_stage *stage, int l, int r, const void *dy, void 
  * backward runs of slice [ctx, ctx+len) (after `warmup` untimed runs) with HIP
  * events and store the medians in nanoseconds at [i_len * n_ctxs + i_ctx] of
  * t_fwd_ns / t_bwd_ns (host arrays).  Entries with len + ctx > max_seq get -1.
- * In DEFERRED mode t_bwd excludes the once-per-sequence weight-gradient GEMMs.
+ * In DEFERRED mode t_bwd excludes the once-per-sequence weight-gradient GEMMs
+ * and bias / LayerNorm-parameter reductions.
  * Synchronous.  Overwrites the K/V cache, the arenas and the parameter
  * gradients with meaningless values: reset and zero them afterwards. */
 tp_status tp_profile_slice_cost(tp_stage *stage, const int *lens, int n_lens, const int *ctxs,

@@ -26,6 +26,9 @@ struct LayerBufs {
   float *dk, *dv; // fp32 [Lmax][H]: gradient reaching each cached key / value
   // per-token output gradients of the four projections (inputs of dW GEMMs)
   void *dy, *dz, *dx1, *dqkv;
+  // per-token LayerNorm output gradients (DEFERRED mode: inputs of the
+  // LayerNorm-parameter gradients, reduced once per sequence)
+  void *du2, *du;
 };
 
 struct Scratch {
@@ -140,6 +143,12 @@ size_t carve(const tp_stage_config* c, void* base, std::vector<LayerBufs>* lbs, 
     b.dz = cv.take(L * F * esz);
     b.dx1 = cv.take(L * H * esz);
     b.dqkv = cv.take(L * 3 * A * esz);
+    if (c->wgrad_mode == TP_WGRAD_DEFERRED) {
+      b.du2 = cv.take(L * H * esz);
+      b.du = cv.take(L * H * esz);
+    } else {
+      b.du2 = b.du = nullptr;
+    }
     if (lbs) lbs->push_back(b);
   }
   Scratch s;
@@ -260,6 +269,32 @@ tp_status wgrad_gemms(tp_stage* S, int li, int l, int n) {
   return TP_OK;
 }
 
+// DEFERRED mode: bias and LayerNorm-parameter gradients of layer li as column
+// reductions over all rows [0, rows) of the kept per-token gradients.
+tp_status deferred_param_reductions(tp_stage* S, int li, int rows) {
+  const int H = S->H, A = S->A, F = S->F, dt = S->dt;
+  const size_t e = S->esz;
+  const double nb = (double)rows * H * e;
+  hipStream_t st = S->stream;
+  LayerBufs& B = S->lb[li];
+  tp_layer_ptrs& G = S->G[li];
+  TRY(launch(S, K_MISC, 0, nb, [&] { return colsum_acc(dt, rows, H, B.dy, H, (float*)G.b_fc2, st); }));
+  TRY(launch(S, K_MISC, 0, (double)rows * F * e,
+             [&] { return colsum_acc(dt, rows, F, B.dz, F, (float*)G.b_fc1, st); }));
+  TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
+    return ln_param_grads(dt, rows, H, B.du2, B.x1, B.mean2, B.rstd2, (float*)G.ln2_g,
+                          (float*)G.ln2_b, st);
+  }));
+  TRY(launch(S, K_MISC, 0, nb, [&] { return colsum_acc(dt, rows, H, B.dx1, H, (float*)G.b_o, st); }));
+  TRY(launch(S, K_MISC, 0, 3.0 * rows * A * e,
+             [&] { return colsum_acc(dt, rows, 3 * A, B.dqkv, 3 * A, (float*)G.b_qkv, st); }));
+  TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
+    return ln_param_grads(dt, rows, H, B.du, B.x_in, B.mean1, B.rstd1, (float*)G.ln1_g,
+                          (float*)G.ln1_b, st);
+  }));
+  return TP_OK;
+}
+
 tp_status forward_impl(tp_stage* S, int l, int r, const void* x, void* y) {
   const int H = S->H, A = S->A, F = S->F, NL = S->cfg.n_layers, dt = S->dt;
   // batch slice: tokens [l, r) of bsz sequences are rows [lr, lr + n)
@@ -327,30 +362,38 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
     GemmArgs g = nn(n, F, H, dyl, H, P.w_fc2);
     g.epi = EPI_DGELU, g.R = rowp(B.z, lr, F, e), g.ldr = F, g.C = rowp(B.dz, lr, F, e), g.ldc = F;
     TRY(run_gemm(S, K_GEMM_DX, g));
-    TRY(launch(S, K_MISC, 0, nb, [&] { return colsum_acc(dt, n, H, dyl, H, (float*)G.b_fc2, st); }));
+    if (per_slice)
+      TRY(launch(S, K_MISC, 0, nb, [&] { return colsum_acc(dt, n, H, dyl, H, (float*)G.b_fc2, st); }));
+    // LayerNorm output gradients: per-slice scratch, or (deferred mode) rows of
+    // per-layer arenas kept for the once-per-sequence parameter reductions
+    void* du2 = per_slice ? S->sc.du2 : rowp(B.du2, lr, H, e);
+    void* du = per_slice ? S->sc.du : rowp(B.du, lr, H, e);
     // FC1 backward: du2 = dz W1
     g = nn(n, H, F, rowp(B.dz, lr, F, e), F, P.w_fc1);
-    g.C = S->sc.du2, g.ldc = H;
+    g.C = du2, g.ldc = H;
     TRY(run_gemm(S, K_GEMM_DX, g));
-    TRY(launch(S, K_MISC, 0, (double)n * F * e, [&] {
-      return colsum_acc(dt, n, F, rowp(B.dz, lr, F, e), F, (float*)G.b_fc1, st);
-    }));
+    if (per_slice)
+      TRY(launch(S, K_MISC, 0, (double)n * F * e, [&] {
+        return colsum_acc(dt, n, F, rowp(B.dz, lr, F, e), F, (float*)G.b_fc1, st);
+      }));
     // LN2 backward + residual: dx1 = dy + LN2^T(du2)
     TRY(launch(S, K_NORM, 0, 4 * nb, [&] {
-      return ln_bwd(dt, n, H, S->sc.du2, rowp(B.x1, lr, H, e), B.mean2 + lr, B.rstd2 + lr, P.ln2_g,
+      return ln_bwd(dt, n, H, du2, rowp(B.x1, lr, H, e), B.mean2 + lr, B.rstd2 + lr, P.ln2_g,
                     dyl, rowp(B.dx1, lr, H, e), st);
     }));
-    TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
-      return ln_param_grads(dt, n, H, S->sc.du2, rowp(B.x1, lr, H, e), B.mean2 + lr, B.rstd2 + lr,
-                            (float*)G.ln2_g, (float*)G.ln2_b, st);
-    }));
+    if (per_slice)
+      TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
+        return ln_param_grads(dt, n, H, du2, rowp(B.x1, lr, H, e), B.mean2 + lr, B.rstd2 + lr,
+                              (float*)G.ln2_g, (float*)G.ln2_b, st);
+      }));
     // output projection backward: dO = dx1 W_o
     g = nn(n, A, H, rowp(B.dx1, lr, H, e), H, P.w_o);
     g.C = S->sc.dout, g.ldc = A;
     TRY(run_gemm(S, K_GEMM_DX, g));
-    TRY(launch(S, K_MISC, 0, nb, [&] {
-      return colsum_acc(dt, n, H, rowp(B.dx1, lr, H, e), H, (float*)G.b_o, st);
-    }));
+    if (per_slice)
+      TRY(launch(S, K_MISC, 0, nb, [&] {
+        return colsum_acc(dt, n, H, rowp(B.dx1, lr, H, e), H, (float*)G.b_o, st);
+      }));
     // attention backward: dq rows, dK/dV into the fp32 buffer for keys [0, r)
     AttnArgs a;
     a.l = l, a.r = r, a.H = A, a.heads = S->heads, a.d = S->d, a.Lmax = S->L;
@@ -371,21 +414,23 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
     }));
     // QKV backward: du = [dq dk dv] W_qkv
     g = nn(n, H, 3 * A, rowp(B.dqkv, lr, 3 * A, e), 3 * A, P.w_qkv);
-    g.C = S->sc.du, g.ldc = H;
+    g.C = du, g.ldc = H;
     TRY(run_gemm(S, K_GEMM_DX, g));
-    TRY(launch(S, K_MISC, 0, 3.0 * n * A * e, [&] {
-      return colsum_acc(dt, n, 3 * A, rowp(B.dqkv, lr, 3 * A, e), 3 * A, (float*)G.b_qkv, st);
-    }));
+    if (per_slice)
+      TRY(launch(S, K_MISC, 0, 3.0 * n * A * e, [&] {
+        return colsum_acc(dt, n, 3 * A, rowp(B.dqkv, lr, 3 * A, e), 3 * A, (float*)G.b_qkv, st);
+      }));
     // LN1 backward + residual: dx = dx1 + LN1^T(du)
     void* out = li == 0 ? dx : rowp(S->lb[li - 1].dy, lr, H, e);
     TRY(launch(S, K_NORM, 0, 4 * nb, [&] {
-      return ln_bwd(dt, n, H, S->sc.du, rowp(B.x_in, lr, H, e), B.mean1 + lr, B.rstd1 + lr, P.ln1_g,
+      return ln_bwd(dt, n, H, du, rowp(B.x_in, lr, H, e), B.mean1 + lr, B.rstd1 + lr, P.ln1_g,
                     rowp(B.dx1, lr, H, e), out, st);
     }));
-    TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
-      return ln_param_grads(dt, n, H, S->sc.du, rowp(B.x_in, lr, H, e), B.mean1 + lr, B.rstd1 + lr,
-                            (float*)G.ln1_g, (float*)G.ln1_b, st);
-    }));
+    if (per_slice)
+      TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
+        return ln_param_grads(dt, n, H, du, rowp(B.x_in, lr, H, e), B.mean1 + lr, B.rstd1 + lr,
+                              (float*)G.ln1_g, (float*)G.ln1_b, st);
+      }));
     if (per_slice) {
       tp_status s = wgrad_gemms(S, li, lr, n);
       if (s != TP_OK) return s;
@@ -393,7 +438,9 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
   }
   if (!per_slice && l == 0 && !S->profiling) {
     for (int li = NL - 1; li >= 0; --li) {
-      tp_status s = wgrad_gemms(S, li, 0, S->cached_len * S->bsz);
+      tp_status s = deferred_param_reductions(S, li, S->cached_len * S->bsz);
+      if (s != TP_OK) return s;
+      s = wgrad_gemms(S, li, 0, S->cached_len * S->bsz);
       if (s != TP_OK) return s;
     }
   }
