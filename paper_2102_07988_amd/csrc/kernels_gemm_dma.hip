@@ -19,6 +19,7 @@
 // compiler's conservative wait-for-all-DMA before LDS reads does not serialise
 // the pipeline.
 #include <algorithm>
+#include <type_traits>
 
 #include "tp_common.hpp"
 #include "tp_kernels.hpp"
@@ -262,6 +263,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
   static_assert(LPT * (STAGES - 2) <= 63, "vmcnt range");
   constexpr bool BLEAD = SB > STAGES;
   static_assert(SB == STAGES || (STAGES == 2 && SB == 3), "unsupported ring shape");
+  static_assert((BK / 16) % 2 == 0, "fragment buffers alternate per k-step across k-tiles");
   constexpr int LPT_B = BK * BN / 8 / NTH;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
@@ -368,41 +370,86 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
     for (int jj = 0; jj < FN; ++jj) asm volatile("" : "+v"(fb[buf][jj]));
   };
 
-  // The k-tile boundary is software-pipelined: the barrier for tile kt+1 and
-  // its first fragment reads come before tile kt's last MFMA step, so those
-  // reads complete while that step runs.  The DMA of the tile after goes out
-  // right after the barrier for split (slice-shaped, weight-streaming)
-  // products, after the last MFMA step for the others; either way into the
-  // stage of tile kt, which every wave finished reading before the barrier.
-  wait_tile(0);
-  issue_next(0);
-  read_frags(0, 0, 0);
-  frags_ready(0);
-  for (int kt = 0; kt < nk; ++kt) {
+  // One k-step runs the FM x FN matrix-core products of fragment buffer `cur`
+  // and, one per product from the first product on, the fragment reads of the
+  // next step into the other buffer, so the reads complete under the products
+  // and the step ends with a single LDS wait.  Scheduling barriers pin that
+  // order: the reads are inline assembly, which the scheduler would otherwise
+  // let the products pass, leaving a wait in front of most of them.
+  //
+  // The k-tile boundary is software-pipelined: half of the last step's
+  // products go out, then the wait and barrier for tile kt+1, then its first
+  // fragment reads interleaved with the other half.  The DMA of the tile after
+  // goes out right after the barrier for split (slice-shaped, weight-streaming)
+  // products, after the last step's products for the others; either way into
+  // the stage of tile kt, which every wave finished reading before the barrier.
+  // The final k-tile is peeled (no next tile to wait for or read), so no
+  // branch inside the loop holds products.
+  constexpr int NR = FM + FN, NM = FM * FN;
+  auto mfma_at = [&](int buf, int t) {
+    const int i = t / FN, j = t % FN;
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+        __builtin_bit_cast(bf16x8_t, fa[buf][i]), __builtin_bit_cast(bf16x8_t, fb[buf][j]),
+        acc[i][j], 0, 0, 0);
+  };
+  auto read_at = [&](int buf, uint32_t ta, uint32_t tb, int k0, int r) {
+    if (r < FM) fa[buf][r] = frag_read<BM, BK, A_KC>(ta, wm0 + 32 * r, k0, lane);
+    else fb[buf][r - FM] = frag_read<BN, BK, B_KC>(tb, wn0 + 32 * (r - FM), k0, lane);
+  };
+  // products [T0, NM) of `cur`; with RD, the reads of `nxt` (tile j, k-offset
+  // k0) one per product from T0 on, any left over after the last product
+  auto interleave = [&](auto t0c, auto rdc, int cur, int nxt, int j, int k0) {
+    constexpr int T0 = decltype(t0c)::value;
+    constexpr bool RD = decltype(rdc)::value;
+    const uint32_t ta = tile_a(j), tb = tile_b(j);
+#pragma unroll
+    for (int t = T0; t < NM; ++t) {
+      if constexpr (RD) {
+        if (t - T0 < NR) read_at(nxt, ta, tb, k0, t - T0);
+      }
+      mfma_at(cur, t);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (RD) {
+#pragma unroll
+      for (int r = NM - T0; r < NR; ++r) read_at(nxt, ta, tb, k0, r);
+    }
+  };
+  using First = std::integral_constant<int, 0>;
+  using Half = std::integral_constant<int, NM / 2>;
+  using Yes = std::integral_constant<bool, true>;
+  using No = std::integral_constant<bool, false>;
+  auto ktile = [&](int kt, auto finalc) {
+    constexpr bool FINAL = decltype(finalc)::value;
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       const int cur = ks & 1, nxt = cur ^ 1;
       const bool last = ks + 1 == BK / 16;
-      bool pending = true;
       if (!last) {
-        read_frags(nxt, kt, 16 * (ks + 1));
-      } else if (kt + 1 < nk) {
+        interleave(First{}, Yes{}, cur, nxt, kt, 16 * (ks + 1));
+      } else if constexpr (!FINAL) {
+#pragma unroll
+        for (int t = 0; t < NM / 2; ++t) mfma_at(cur, t);
+        __builtin_amdgcn_sched_barrier(0);
         wait_tile(kt + 1);
         if (SPLIT) issue_next(kt + 1);
-        read_frags(nxt, kt + 1, 0);
+        interleave(Half{}, Yes{}, cur, nxt, kt + 1, 0);
       } else {
-        pending = false;
+        interleave(First{}, No{}, cur, nxt, 0, 0);
       }
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              __builtin_bit_cast(bf16x8_t, fa[cur][i]), __builtin_bit_cast(bf16x8_t, fb[cur][j]),
-              acc[i][j], 0, 0, 0);
-      if (!SPLIT && last && kt + 1 < nk) issue_next(kt + 1);
-      if (pending) frags_ready(nxt);
+      __builtin_amdgcn_sched_barrier(0);
+      if (!FINAL && !SPLIT && last) issue_next(kt + 1);
+      if (!(FINAL && last)) frags_ready(nxt);
     }
+  };
+
+  wait_tile(0);
+  issue_next(0);
+  read_frags(0, 0, 0);
+  frags_ready(0);
+  if (nk > 0) {
+    for (int kt = 0; kt + 1 < nk; ++kt) ktile(kt, No{});
+    ktile(nk - 1, Yes{});
   }
   // every outstanding DMA has been waited for: the last iteration waited for 0
 
@@ -609,10 +656,10 @@ hipError_t run_cfg_id(int cfg, const GemmArgs& a, hipStream_t s, int splits = 0)
 // fitted (log least squares, rms error 9 %) to a sweep of every candidate on
 // the stage's products for hidden sizes 2048-12288, operation-partitioning
 // shards and 128-512 rows:
-//   t = max(rounds * (0.68 + kt * c_kt), rows_tiles * N * K * 2 B * 0.178 us/MB)
-//       + (splits > 1 ? 5.5 + splits * M * N * 8 B / 5.8 MB/us : 0)
+//   t = max(rounds * (0.73 + kt * c_kt), rows_tiles * N * K * 2 B * 0.180 us/MB)
+//       + (splits > 1 ? 5.6 + splits * M * N * 8 B / 5.7 MB/us : 0)
 // with rounds = workgroups / 256 rounded up, kt = k-tiles per split and c_kt
-// = 0.62 / 0.98 / 1.60 us for 128x128 / 256x128 / 256x256 tiles: a round of
+// = 0.60 / 0.92 / 1.45 us for 128x128 / 256x128 / 256x256 tiles: a round of
 // workgroups, not below the weight stream from HBM, plus the partial sums.
 struct TileChoice {
   int cfg, splits;
@@ -623,20 +670,20 @@ TileChoice choose_tiles(const GemmArgs& a) {
     int cfg, bm, bn;
     double c_kt;
   };
-  static const Cand kCands[] = {{0, 128, 128, 0.6208}, {1, 256, 128, 0.9844}, {3, 256, 256, 1.601}};
+  static const Cand kCands[] = {{0, 128, 128, 0.6001}, {1, 256, 128, 0.9215}, {3, 256, 256, 1.4538}};
   const int nkt = a.K / 64;
   double best = 1e300;
   TileChoice pick{3, 1};
   for (const Cand& c : kCands) {
     const long mt = cdiv(a.M, c.bm), tiles = mt * cdiv(a.N, c.bn);
-    const double hbm = (double)mt * a.N * a.K * 2.0 / 1e6 * 0.1783;
+    const double hbm = (double)mt * a.N * a.K * 2.0 / 1e6 * 0.1796;
     for (int sp : kSplits) {
       if (sp > nkt) break;
       if (sp > 1 && (!a.ws || (long)sp * a.M * a.N > a.ws_elems)) break;
       const int ks = cdiv(nkt, sp), s = cdiv(nkt, ks);
       const long rounds = cdiv(tiles * s, 256);
-      double t = std::max(rounds * (0.6789 + ks * c.c_kt), hbm);
-      if (s > 1) t += 5.5466 + (double)s * a.M * a.N * 8.0 / 1e6 / 5.7959;
+      double t = std::max(rounds * (0.7342 + ks * c.c_kt), hbm);
+      if (s > 1) t += 5.5925 + (double)s * a.M * a.N * 8.0 / 1e6 / 5.7014;
       if (t < best) {
         best = t;
         pick = {c.cfg, s};
