@@ -47,8 +47,18 @@ __device__ inline int swz_kc(int r) {
   if constexpr (BK == 64) return (r ^ (r >> 3)) & 7;
   else return (r >> 2) & 3;
 }
-// m/n-contiguous tile of R columns: k-row k, 16-byte chunk c at k*2R + 16*(c ^ swz_mc(k)).
-__device__ inline int swz_mc(int k) { return (k & 3) << 2; }
+// m/n-contiguous tile of R columns: k-row k, 16-byte chunk c at k*2R + 16*(c ^ swz_mc<R>(k)).
+// A transposing read takes 32 bytes from each of 4 consecutive k-rows.  Rows of
+// 256 or 512 bytes all start on bank 0, so the row's chunk index is XORed with
+// 4 (k mod 4) (64-byte steps); rows of 384 bytes (R = 192) already alternate
+// between bank 0 and bank 32, so XOR 4 on rows 2 and 3 of each 4 suffices and
+// keeps the 24 chunks of a row within range.
+template <int R>
+__device__ inline int swz_mc(int k) {
+  static_assert(R % 128 == 0 || R == 192, "transposing-read swizzle needs R = 128 j or 192");
+  if constexpr (R == 192) return ((k >> 1) & 1) << 2;
+  else return (k & 3) << 2;
+}
 
 template <typename T, int EPI>
 __device__ inline void epi_store(const GemmArgs& a, int m, int n, float acc) {
@@ -150,7 +160,7 @@ struct DmaPlan {
       } else {
         constexpr int CPR = R / 8;  // chunks per k-row
         const int krow = s / CPR, phys = s % CPR;
-        const int logical = phys ^ swz_mc(krow);
+        const int logical = phys ^ swz_mc<R>(krow);
         const int gc = min(r0 + logical * 8, rmax - 8);
         off[i] = (uint32_t)(((long)krow * ld + gc) * 2);
       }
@@ -189,11 +199,11 @@ __device__ inline u32x4 frag_read(uint32_t tile, int rc_base, int k0, int lane) 
     u32x2 lo, hi;
     {
       const int kr = kr0;
-      lo = ds_read_tr(tile + kr * (2 * R) + (((col >> 3) ^ swz_mc(kr)) << 4) + ((col & 7) << 1));
+      lo = ds_read_tr(tile + kr * (2 * R) + (((col >> 3) ^ swz_mc<R>(kr)) << 4) + ((col & 7) << 1));
     }
     {
       const int kr = kr0 + 4;
-      hi = ds_read_tr(tile + kr * (2 * R) + (((col >> 3) ^ swz_mc(kr)) << 4) + ((col & 7) << 1));
+      hi = ds_read_tr(tile + kr * (2 * R) + (((col >> 3) ^ swz_mc<R>(kr)) << 4) + ((col & 7) << 1));
     }
     u32x4 r;
     r.x = lo.x;
@@ -259,6 +269,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
   constexpr int TILE_A = BM * BK, TILE_B = BN * BK, STAGE = TILE_A + TILE_B;  // elements
   constexpr int LPT = BK * (BM + BN) / 8 / NTH;  // DMA instructions per thread per k-tile
   static_assert(FM >= 1 && FN >= 1, "wave tile below 32 x 32");
+  static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile not a multiple of 32 x 32");
   static_assert((BK * BM / 8) % NTH == 0 && (BK * BN / 8) % NTH == 0, "uneven DMA split");
   static_assert(LPT * (STAGES - 2) <= 63, "vmcnt range");
   constexpr bool BLEAD = SB > STAGES;
@@ -646,6 +657,10 @@ hipError_t run_cfg_id(int cfg, const GemmArgs& a, hipStream_t s, int splits = 0)
     case 1: return run_dma<256, 128, 64, 4, 2, A_KC, B_KC, 3>(a, s, splits);
     case 2: return run_dma<256, 256, 64, 2, 4, A_KC, B_KC, 2>(a, s, splits);
     case 3: return run_dma<256, 256, 64, 2, 4, A_KC, B_KC, 2, 3>(a, s, splits);
+    case 4:
+      // 256 x 192: 256 tiles for a 256-row product of width 49152, 64 for 12288
+      if constexpr (A_KC) return run_dma<256, 192, 64, 4, 2, A_KC, B_KC, 2, 3>(a, s, splits);
+      else return hipErrorNotSupported;
     default: return hipErrorNotSupported;
   }
 }
@@ -653,13 +668,13 @@ hipError_t run_cfg_id(int cfg, const GemmArgs& a, hipStream_t s, int splits = 0)
 // Tile shape and split count for a product whose A operand is k-contiguous
 // (slice activations or output gradients times a weight matrix): the
 // candidate (tiles, splits) with the smallest modelled time.  The model was
-// fitted (log least squares, rms error 9 %) to a sweep of every candidate on
+// fitted (log least squares, rms error 10 %) to a sweep of every candidate on
 // the stage's products for hidden sizes 2048-12288, operation-partitioning
 // shards and 128-512 rows:
-//   t = max(rounds * (0.73 + kt * c_kt), rows_tiles * N * K * 2 B * 0.180 us/MB)
-//       + (splits > 1 ? 5.6 + splits * M * N * 8 B / 5.7 MB/us : 0)
+//   t = max(rounds * (0.74 + kt * c_kt), rows_tiles * N * K * 2 B * 0.177 us/MB)
+//       + (splits > 1 ? 5.7 + splits * M * N * 8 B / 5.8 MB/us : 0)
 // with rounds = workgroups / 256 rounded up, kt = k-tiles per split and c_kt
-// = 0.60 / 0.92 / 1.45 us for 128x128 / 256x128 / 256x256 tiles: a round of
+// = 0.59 / 0.91 / 1.21 / 1.44 us for 128x128 / 256x128 / 256x192 / 256x256 tiles: a round of
 // workgroups, not below the weight stream from HBM, plus the partial sums.
 struct TileChoice {
   int cfg, splits;
@@ -670,20 +685,21 @@ TileChoice choose_tiles(const GemmArgs& a) {
     int cfg, bm, bn;
     double c_kt;
   };
-  static const Cand kCands[] = {{0, 128, 128, 0.6001}, {1, 256, 128, 0.9215}, {3, 256, 256, 1.4538}};
+  static const Cand kCands[] = {
+      {0, 128, 128, 0.5931}, {1, 256, 128, 0.9088}, {4, 256, 192, 1.2088}, {3, 256, 256, 1.4367}};
   const int nkt = a.K / 64;
   double best = 1e300;
   TileChoice pick{3, 1};
   for (const Cand& c : kCands) {
     const long mt = cdiv(a.M, c.bm), tiles = mt * cdiv(a.N, c.bn);
-    const double hbm = (double)mt * a.N * a.K * 2.0 / 1e6 * 0.1796;
+    const double hbm = (double)mt * a.N * a.K * 2.0 / 1e6 * 0.1773;
     for (int sp : kSplits) {
       if (sp > nkt) break;
       if (sp > 1 && (!a.ws || (long)sp * a.M * a.N > a.ws_elems)) break;
       const int ks = cdiv(nkt, sp), s = cdiv(nkt, ks);
       const long rounds = cdiv(tiles * s, 256);
-      double t = std::max(rounds * (0.7342 + ks * c.c_kt), hbm);
-      if (s > 1) t += 5.5925 + (double)s * a.M * a.N * 8.0 / 1e6 / 5.7014;
+      double t = std::max(rounds * (0.7377 + ks * c.c_kt), hbm);
+      if (s > 1) t += 5.6764 + (double)s * a.M * a.N * 8.0 / 1e6 / 5.7874;
       if (t < best) {
         best = t;
         pick = {c.cfg, s};
