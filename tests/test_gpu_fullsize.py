@@ -8,7 +8,10 @@ slicing), on the same seeded inputs it draws on the device.
   stage (hidden 12288, 96 heads) at L = 2048 (8 x 256) and L = 8192
   (16 x 512): the oracle is too slow for the whole sequence, so
   (a) stage outputs y of tokens 0..15, which by the causal mask depend on
-  x[0..15] only, against the oracle run on those 16 tokens; (b) properties that
+  x[0..15] only, against the oracle run on those 16 tokens; (c) sampled later
+  rows (slice edges, long prefixes, seeded random tokens) against the
+  row-sampling oracle (fp64 library matrix products over tokens 0..max row,
+  pinned to the slice oracle in test_oracle_rows.py); (b) properties that
   hold at any size: the last layer's FC2 bias gradient equals the column sums
   of dy; per-slice and deferred weight gradients agree to fp32 summation order
   with y and dx bit-identical; a different backward slicing gives the same
@@ -20,6 +23,7 @@ import numpy as np
 import pytest
 import torch
 
+from oracle.rows import stage_output_rows
 from paper_2102_07988_amd import synth
 from stage_harness import PARAM_KEYS, compare, rel_l2, run_oracle
 
@@ -103,8 +107,50 @@ def test_large_stage_bench_configuration(H, heads, L, slice_len):
     n = 16
     p64 = synth.params_f64([{k: v.cpu() for k, v in p.items()} for p in params])
     ost = OracleStage(p64, H, heads, n)
-    del p64
     y_ref = ost.forward(0, n, synth.to_f64(x[:n].cpu()))
+    del ost
     err = rel_l2(y[:n].float().cpu().numpy(), y_ref)
     print(f"  y[0:16] vs oracle: {err:.2e}", flush=True)
     assert err < TOL_BF16
+
+    # (c) late rows (last and first token of slices, long prefixes, a few seeded
+    # random ones) against the row-sampling oracle, which evaluates the causal
+    # stage for tokens 0..max(rows) in fp64; the 8192-token case stops at 6144
+    # tokens to bound the host's fp64 work
+    T = min(L, 6144)
+    rows = sorted({slice_len - 1, slice_len, T // 2 - 1, T // 2, T - slice_len, T - 1}
+                  | set(np.random.default_rng(L + H).integers(16, T, size=3).tolist()))
+    y_rows = stage_output_rows(p64, synth.to_f64(x[:T].cpu()), heads, rows)
+    del p64
+    gc.collect()
+    err = rel_l2(y[rows].float().cpu().numpy(), y_rows)
+    print(f"  y{rows} vs row oracle: {err:.2e}", flush=True)
+    assert err < TOL_BF16
+
+
+def test_fp32_validation_mode_full_175b_rows():
+    """The fp32 validation mode at the GPT-3-175B stage shape (2 layers, hidden
+    12288, 96 heads, L = 2048, 8 x 256 slices): sampled output rows against the
+    row-sampling oracle within 1e-4, so the bf16 path's larger error at this size
+    is its rounding, not the algorithm."""
+    from paper_2102_07988_amd import terapipe as tp
+    n_layers, H, heads, L, n = 2, 12288, 96, 2048, 256
+    print(f"case fp32 validation: H={H} heads={heads} L={L} 8x{n} forward", flush=True)
+    dev = torch.device("cuda:0")
+    params = synth.stage_params(n_layers, H, seed=synth.SEED_PARAMS, dtype=torch.float32,
+                                device=dev)
+    x = synth.hidden_states(L, H, seed=synth.SEED_X, dtype=torch.float32, device=dev)
+    st = tp.Stage(params, H, heads, L, dtype="fp32", wgrad="deferred")
+    y = torch.empty_like(x)
+    for l in range(0, L, n):
+        st.forward(l, l + n, x[l:l + n], out=y[l:l + n])
+    torch.cuda.synchronize()
+    del st
+    rows = [0, 7, n - 1, n, 1023, 1024, 1536, L - n, L - 1]
+    p64 = synth.params_f64([{k: v.cpu() for k, v in p.items()} for p in params])
+    del params
+    gc.collect()
+    y_rows = stage_output_rows(p64, synth.to_f64(x.cpu()), heads, rows)
+    err = rel_l2(y[rows].double().cpu().numpy(), y_rows)
+    print(f"  fp32 y{rows} vs row oracle: {err:.2e}", flush=True)
+    assert err < 1e-4
