@@ -19,6 +19,7 @@
 // compiler's conservative wait-for-all-DMA before LDS reads does not serialise
 // the pipeline.
 #include <algorithm>
+#include <atomic>
 #include <type_traits>
 
 #include "tp_common.hpp"
@@ -569,15 +570,20 @@ hipError_t launch_dma(const GemmArgs& a, hipStream_t s) {
         (cdiv(cdiv(a.M, BM), TileWalk::SM) * cdiv(cdiv(a.N, BN), TileWalk::SN) + 7) / 8;
     grid = dim3(rounds * 8 * WALK_PER_XCD, 1, 1);
   }
+  // the dynamic-LDS limit is raised once per kernel and device (bit d of a
+  // per-kernel mask; devices past 31 set it on every launch)
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) dev = 32;
 #define TP_LAUNCH(E)                                                                         \
   do {                                                                                       \
     auto* fn = gemm_dma_kernel<BM, BN, BK, WGM, WGN, A_KC, B_KC, E, SPLIT, STAGES, SB>;    \
-    static bool attr = false;                                                                \
-    if (!attr) {                                                                             \
+    static std::atomic<uint32_t> attr_set{0};                                                \
+    const uint32_t bit = dev < 32 ? 1u << dev : 0u;                                          \
+    if (!bit || !(attr_set.load(std::memory_order_acquire) & bit)) {                         \
       hipError_t e = hipFuncSetAttribute((const void*)fn,                                    \
                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds); \
       if (e != hipSuccess) return e;                                                         \
-      attr = true;                                                                           \
+      attr_set.fetch_or(bit, std::memory_order_release);                                     \
     }                                                                                        \
     fn<<<grid, NTH, lds, s>>>(a);                                                            \
   } while (0)
