@@ -8,9 +8,10 @@ second: per layer and slice, 24 n H^2 (projections) + 4 H per causal
 (query, key <= query) pair forward, backward twice forward.
 
 Prints one JSON line.  Per-kernel-class times are measured with HIP events on
-the stage's stream over the timed region; `roofline` reports the class with
-the largest total time.  `cpu_baseline` times the fp64 CPU oracle on a bounded
-sample of the same workload (one layer, a short slice).
+the stage's stream; `roofline` reports one kernel: the deferred dW GEMM (the
+largest single kernel) in the deferred mode, else the class with the largest
+total time.  `cpu_baseline` times the fp64 CPU oracle on a bounded sample of
+the same workload (one layer, a short slice).
 """
 from __future__ import annotations
 
