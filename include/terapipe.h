@@ -101,7 +101,10 @@ typedef struct tp_stage tp_stage;
  * invalid.  Host only. */
 size_t tp_stage_workspace_bytes(const tp_stage_config *cfg);
 
-/* Create a stage.  params / grads: arrays of cfg->n_layers entries.
+/* Create a stage: one pipeline cell, the run of consecutive layers that one
+ * device holds and runs over every slice of a sequence (Sec. 3.2; the cell
+ * partition of the layers is the unit of the pipeline in Sec. 3.3).
+ * params / grads: arrays of cfg->n_layers entries.
  * workspace: >= tp_stage_workspace_bytes(cfg) bytes of device memory,
  * 256-byte aligned, owned by the caller and used only by this stage until
  * tp_stage_destroy.  stream: a hipStream_t (NULL = default stream) on which
@@ -118,19 +121,30 @@ void tp_stage_destroy(tp_stage *stage);
 
 /* Start a new sequence: no cached tokens, backward frontier 0, and the fp32
  * dK/dV buffer zeroed (enqueued on the stream; a fill kernel, no memset node).
+ * This is the empty prefix state of Eq. 2: the keys and values of positions
+ * before the first slice, which every later slice's attention sums over,
+ * start out empty (Sec. 3.2: the cell keeps them from slice to slice).
  * Parameter gradients are not touched. */
 tp_status tp_kv_prefix_reset(tp_stage *stage);
 
 /* Forward of token slice [l, r) through every layer (Sec. 3.2).
  * x: [r-l][b][H] stage input rows, y: [r-l][b][H] stage output rows (stage
- * dtype, device; b = cfg.batch, token-major).  Requires 0 <= l < r <= max_seq (else TP_ERR_INVALID) and l equal to
- * the number of cached tokens (else TP_ERR_ORDER).  Appends the slice's keys
+ * dtype, device; b = cfg.batch, token-major).  Requires 0 <= l < r <= max_seq
+ * (else TP_ERR_INVALID), l equal to the number of cached tokens and no
+ * backward call since the last tp_kv_prefix_reset (else TP_ERR_ORDER: a
+ * slice's backward needs the forward of every later slice, so a forward after
+ * backward has begun is misuse).  Appends the slice's keys
  * and values to each layer's cache, saves what backward needs, and sets the
  * cached length and the backward frontier to r.  x and y must not overlap and
  * must be 16-byte aligned (else TP_ERR_INVALID). */
 tp_status tp_slice_forward(tp_stage *stage, int l, int r, const void *x, void *y);
 
 /* Backward of token slice [l, r) through every layer, in reverse layer order.
+ * The backward pass of a cell runs over the slices in the reverse of their
+ * forward order (the last paragraph of Sec. 3.3 applies the same slicing
+ * analysis to the backward time t_bwd; Sec. 3.2 for the cell pipeline):
+ * gradients that a slice's queries send to earlier positions' keys and values
+ * must be complete before those positions' own backward runs.
  * dy: [r-l][b][H] gradient of the stage output rows, dx: [r-l][b][H] gradient
  * of the stage input rows (stage dtype, device).  Requires 0 <= l < r and r equal to
  * the backward frontier (slices arrive in reverse order; their boundaries need
@@ -244,7 +258,10 @@ const char *tp_status_string(tp_status status);
  * events on the stage stream; tp_stage_kernel_stats synchronises the stream
  * and returns, per class, the number of launches, their summed duration and
  * their summed algorithmic flop and HBM-byte counts since the last reset of
- * the counters.  Returns the number of classes written (<= cap). */
+ * the counters.  Returns the number of classes written (<= cap), or -1 when
+ * the stream or an event could not be read (events recorded under stream
+ * capture cannot be): the pending timings are then dropped and the counters
+ * reset.  Launches captured into a graph are not timed by this mechanism. */
 typedef struct {
   char name[48];
   int64_t launches;

@@ -1,5 +1,6 @@
 // Kernel selection: the bf16 fast kernels where they cover the shape, the
 // generic kernels otherwise (and for the fp32 validation mode).
+#include "tp_common.hpp"
 #include "tp_kernels.hpp"
 
 namespace tp {
@@ -11,6 +12,7 @@ hipError_t gemm_mfma_bf16(const GemmArgs& a, hipStream_t s);
 hipError_t gemm_dma_bf16(const GemmArgs& a, hipStream_t s);
 
 hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s) {
+  clear_stale_error();
   if (dtype == DT_BF16) {
     hipError_t e = gemm_dma_bf16(a, s);
     if (e != hipErrorNotSupported) return e;
@@ -24,6 +26,7 @@ hipError_t attn_fwd_mfma_bf16(const AttnArgs& a, hipStream_t s);
 hipError_t attn_bwd_mfma_bf16(const AttnArgs& a, hipStream_t s);
 
 hipError_t attn_fwd(int dtype, const AttnArgs& a, hipStream_t s) {
+  clear_stale_error();
   if (dtype == DT_BF16) {
     const hipError_t e = attn_fwd_mfma_bf16(a, s);
     if (e != hipErrorNotSupported) return e;
@@ -32,6 +35,7 @@ hipError_t attn_fwd(int dtype, const AttnArgs& a, hipStream_t s) {
 }
 
 hipError_t attn_bwd(int dtype, const AttnArgs& a, hipStream_t s) {
+  clear_stale_error();
   if (dtype == DT_BF16) {
     const hipError_t e = attn_bwd_mfma_bf16(a, s);
     if (e != hipErrorNotSupported) return e;

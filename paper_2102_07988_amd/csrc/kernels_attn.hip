@@ -356,16 +356,17 @@ __global__ __launch_bounds__(256) void attn_bwd_rowdot(AttnArgs a0) {
 
 // ------------------------------------------------------------ dK / dV
 
-// MODE 0: dK and dV; 1: dV only (S, P, dV += P^T dO); 2: dK only (S, dP, dS,
-// dK += dS^T Q).  The single-output modes hold one accumulator set and fit
-// two waves per SIMD; together they recompute S once more than mode 0.
+// MODE 1: dV (S, P, dV += P^T dO); MODE 2: dK (S, dP, dS, dK += dS^T Q).
+// Each holds one accumulator set and fits two waves per SIMD; the pair
+// recomputes S once more than a kernel forming both would.
 // ST query tiles form the LDS ring: tile qb + ST - 1 is requested while tile
 // qb is multiplied.
 template <int D, int NW, int MODE, int ST>
-__global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma(AttnArgs a0) {
+__global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dkdv_mfma(AttnArgs a0) {
+  static_assert(MODE == 1 || MODE == 2, "dV (1) or dK (2)");
   const AttnArgs a = attn_seq_view<uint16_t>(a0);
   using T = Tile<D>;
-  constexpr bool DO_K = MODE != 1, DO_V = MODE != 2;
+  constexpr bool DO_K = MODE == 2, DO_V = MODE == 1;
   constexpr int NTH = 64 * NW, BQ = 32, KS = D / 16, JB = D / 32;
   constexpr int TILE = BQ * D;                           // elements
   constexpr int STAGE = 2 * TILE + NW * 128;             // Q, dO, then per-wave [lse | D]
@@ -382,19 +383,15 @@ __global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma
   const uint16_t* dO = (const uint16_t*)a.dout + h * D;
   const uint32_t sbase = lds_addr(smem);
 
-  // K fragments of the wave's keys stay in registers; V fragments (dK needs
-  // them for dP) too in mode 0, while the dK-only mode keeps the block's V
-  // rows in LDS (loaded once, after the query-tile ring) and reads them per
-  // query block
-  constexpr bool V_RESIDENT = MODE == 0, V_LDS = MODE == 2;
-  u32x4 kf[KS], vf[KS];
+  // K fragments of the wave's keys stay in registers; the dK kernel keeps
+  // the block's V rows (needed for dP) in LDS, loaded once after the
+  // query-tile ring, and reads them per query block
+  constexpr bool V_LDS = MODE == 2;
+  u32x4 kf[KS];
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) {
-    kf[kk] = vf[kk] = u32x4{0, 0, 0, 0};
-    if (s_me < a.r) {
-      kf[kk] = *(const u32x4*)(Kc + (long)s_me * H + 16 * kk + 8 * G);
-      if constexpr (V_RESIDENT) vf[kk] = *(const u32x4*)(Vc + (long)s_me * H + 16 * kk + 8 * G);
-    }
+    kf[kk] = u32x4{0, 0, 0, 0};
+    if (s_me < a.r) kf[kk] = *(const u32x4*)(Kc + (long)s_me * H + 16 * kk + 8 * G);
   }
   f32x16_t dk[JB], dv[JB];
 #pragma unroll
@@ -475,18 +472,7 @@ __global__ __launch_bounds__(64 * NW, MODE == 0 ? 1 : 2) void attn_bwd_dkdv_mfma
 #pragma unroll
         for (int b = 0; b < 4; ++b) dq4[b] = ds_read128(LD + 128 + (8 * b + 4 * G) * 4);
       }
-      if constexpr (DO_K && V_RESIDENT) {
-        u32x4 oa[KS];
-#pragma unroll
-        for (int kk = 0; kk < KS; ++kk) oa[kk] = T::row8(Ot, c, 2 * kk + G);
-        lgkm_wait(oa[0]);
-#pragma unroll
-        for (int kk = 1; kk < KS; ++kk) lgkm_tie(oa[kk]);
-#pragma unroll
-        for (int b = 0; b < 4; ++b) lgkm_tie(dq4[b]);
-#pragma unroll
-        for (int kk = 0; kk < KS; ++kk) dp = mfma(oa[kk], vf[kk], dp);
-      } else if constexpr (DO_K) {
+      if constexpr (DO_K) {
         // dP = dO V^T in two halves of the head width, V rows from LDS (rows
         // of keys >= r repeat the last key; their scores are masked)
 #pragma unroll
@@ -811,12 +797,6 @@ void plan_split(AttnArgs& a, bool with_ml) {
   a.kv_chunk = cdiv(cdiv(a.r, ns), 64) * 64;
   a.nsplit = cdiv(a.r, a.kv_chunk);
 }
-// dK/dV as one kernel (0) or as a dV kernel (1) followed by a dK kernel (2)
-#ifndef TP_DKDV_MODE_A
-#define TP_DKDV_MODE_A 1
-#endif
-constexpr int DKDV_MODE_A = TP_DKDV_MODE_A;
-
 template <typename K>
 hipError_t set_lds(K* fn, size_t bytes) {
   if (bytes <= 64 * 1024) return hipSuccess;
@@ -859,11 +839,11 @@ hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
   // the block's V rows stay in LDS; with head width 128 it runs 8 waves (256
   // keys) over a 4-tile ring (137 KB, one block per CU), with 64 4 waves over
   // a 2-tile ring.
-  constexpr int STA = DKDV_MODE_A == 0 ? 2 : 4;
+  constexpr int STA = 4;
   constexpr int NWK = D == 128 ? 8 : 4, STK = D == 128 ? 4 : 2;
   constexpr size_t lds_a = STA * (2 * 32 * D + NWF * 128) * 2;
   constexpr size_t lds_k = STK * (2 * 32 * D + NWK * 128) * 2 + 32 * NWK * D * 2;
-  if (DKDV_MODE_A != 0 && (long)cdiv(a.r, 32 * NWF) * a.heads * a.bs < 128) {
+  if ((long)cdiv(a.r, 32 * NWF) * a.heads * a.bs < 128) {
     // few key blocks (few heads, short prefix): two-wave dV blocks and
     // four-wave dK blocks over two-tile rings, so more blocks share the CUs
     constexpr size_t lds_v2 = 2 * (2 * 32 * D + 2 * 128) * 2;
@@ -880,20 +860,18 @@ hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
     return dq_d<D>(a, s);
   }
-  e = set_lds(attn_bwd_dkdv_mfma<D, NWF, DKDV_MODE_A, STA>, lds_a);
+  e = set_lds(attn_bwd_dkdv_mfma<D, NWF, 1, STA>, lds_a);
   if (e != hipSuccess) return e;
-  attn_bwd_dkdv_mfma<D, NWF, DKDV_MODE_A, STA>
+  attn_bwd_dkdv_mfma<D, NWF, 1, STA>
       <<<dim3(cdiv(a.r, 32 * NWF), a.heads, a.bs), 64 * NWF, lds_a, s>>>(a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if constexpr (DKDV_MODE_A != 0) {
-    e = set_lds(attn_bwd_dkdv_mfma<D, NWK, 2, STK>, lds_k);
-    if (e != hipSuccess) return e;
-    attn_bwd_dkdv_mfma<D, NWK, 2, STK>
-        <<<dim3(cdiv(a.r, 32 * NWK), a.heads, a.bs), 64 * NWK, lds_k, s>>>(a);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
+  e = set_lds(attn_bwd_dkdv_mfma<D, NWK, 2, STK>, lds_k);
+  if (e != hipSuccess) return e;
+  attn_bwd_dkdv_mfma<D, NWK, 2, STK>
+      <<<dim3(cdiv(a.r, 32 * NWK), a.heads, a.bs), 64 * NWK, lds_k, s>>>(a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
   return dq_d<D>(a, s);
 }
 

@@ -506,6 +506,7 @@ __global__ void copy_kernel(size_t n, const T* src, T* dst) {
 
 hipError_t ln_fwd(int dtype, int n, int H, const void* x, void* x_copy, const void* g,
                   const void* b, void* u, float* mean, float* rstd, float eps, hipStream_t s) {
+  clear_stale_error();
   if (n <= 0) return hipSuccess;
   const LnShape sh = ln_shape(H);
 #define TP_LN(TT, C)                                                                        \
@@ -522,6 +523,7 @@ hipError_t ln_fwd(int dtype, int n, int H, const void* x, void* x_copy, const vo
 
 hipError_t ln_bwd(int dtype, int n, int H, const void* du, const void* x, const float* mean,
                   const float* rstd, const void* g, const void* resid, void* dx, hipStream_t s) {
+  clear_stale_error();
   if (n <= 0) return hipSuccess;
   const LnShape sh = ln_shape(H);
 #define TP_LN(TT, C)                                                                        \
@@ -539,6 +541,7 @@ hipError_t ln_bwd(int dtype, int n, int H, const void* du, const void* x, const 
 hipError_t ln_param_grads(int dtype, int n, int H, const void* du, const void* x,
                           const float* mean, const float* rstd, float* dg, float* db,
                           hipStream_t s) {
+  clear_stale_error();
   if (n <= 0) return hipSuccess;
   const int blocks = cdiv(H, CR_COLS);
   if (dtype == DT_FP32)
@@ -552,6 +555,7 @@ hipError_t ln_param_grads(int dtype, int n, int H, const void* du, const void* x
 
 hipError_t colsum_acc(int dtype, int n, int N, const void* A, long lda, float* out,
                       hipStream_t s) {
+  clear_stale_error();
   if (n <= 0 || N <= 0) return hipSuccess;
   const int blocks = cdiv(N, CR_COLS);
   if (dtype == DT_FP32)
@@ -563,6 +567,7 @@ hipError_t colsum_acc(int dtype, int n, int N, const void* A, long lda, float* o
 
 hipError_t pack_dkv(int dtype, int n, int H, const float* dk, const float* dv, void* dqkv,
                     hipStream_t s) {
+  clear_stale_error();
   const long tot = (long)n * (H / 8);
   if (tot <= 0) return hipSuccess;
   auto al = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
@@ -575,6 +580,7 @@ hipError_t pack_dkv(int dtype, int n, int H, const float* dk, const float* dv, v
 }
 
 hipError_t fill_f32(float* p, size_t n, float v, hipStream_t s) {
+  clear_stale_error();
   if (n == 0) return hipSuccess;
   const int blocks = (int)((n + 255) / 256 < 8192 ? (n + 255) / 256 : 8192);
   fill_f32_kernel<<<blocks, 256, 0, s>>>(p, n, v);
@@ -582,6 +588,7 @@ hipError_t fill_f32(float* p, size_t n, float v, hipStream_t s) {
 }
 
 hipError_t copy_rows(int dtype, int n, int H, const void* src, void* dst, hipStream_t s) {
+  clear_stale_error();
   const size_t tot = (size_t)n * H;
   if (tot == 0) return hipSuccess;
   const int blocks = (int)((tot + 255) / 256 < 8192 ? (tot + 255) / 256 : 8192);

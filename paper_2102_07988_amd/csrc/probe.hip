@@ -56,15 +56,19 @@ extern "C" tp_status tp_measure_mfma_peak(void* stream, int iters, void* sink,
     return TP_ERR_HIP;
   }
   tp_status st = TP_OK;
+  (void)hipGetLastError();  // drop an error an earlier, unrelated call left behind
   mfma_chain_kernel<<<grid, 256, 0, s>>>(iters, (float*)sink);  // warm-up
-  hipEventRecord(e0, s);
-  mfma_chain_kernel<<<grid, 256, 0, s>>>(iters, (float*)sink);
-  hipEventRecord(e1, s);
-  if (hipGetLastError() != hipSuccess || hipEventSynchronize(e1) != hipSuccess) {
+  bool ok = hipGetLastError() == hipSuccess && hipEventRecord(e0, s) == hipSuccess;
+  if (ok) {
+    mfma_chain_kernel<<<grid, 256, 0, s>>>(iters, (float*)sink);
+    ok = hipGetLastError() == hipSuccess;
+  }
+  float ms = 0.f;
+  ok = ok && hipEventRecord(e1, s) == hipSuccess && hipEventSynchronize(e1) == hipSuccess &&
+       hipEventElapsedTime(&ms, e0, e1) == hipSuccess && ms > 0.f;
+  if (!ok) {
     st = TP_ERR_HIP;
   } else {
-    float ms = 0.f;
-    hipEventElapsedTime(&ms, e0, e1);
     const double flops = (double)grid * 4 * iters * 8 * (2.0 * 32 * 32 * 16);
     *tflops = flops / (ms * 1e-3) / 1e12;
   }

@@ -189,17 +189,28 @@ hipEvent_t get_event(tp_stage* S) {
   return e;
 }
 
-// Run one launch, bracketed by events when timing is on.
+// Run one launch, bracketed by events when timing is on.  A failed event call
+// fails the launch (its status is returned; the events go back to the pool).
 template <typename Fn>
 hipError_t launch(tp_stage* S, int cls, double flops, double bytes, Fn&& fn) {
   if (!S->timing) return fn();
-  hipEvent_t a = get_event(S), b = get_event(S);
-  if (!a || !b) return hipErrorOutOfMemory;
-  hipEventRecord(a, S->stream);
-  hipError_t e = fn();
-  hipEventRecord(b, S->stream);
+  hipEvent_t a = get_event(S);
+  if (!a) return hipErrorOutOfMemory;
+  hipEvent_t b = get_event(S);
+  if (!b) {
+    S->free_events.push_back(a);
+    return hipErrorOutOfMemory;
+  }
+  hipError_t e = hipEventRecord(a, S->stream);
+  if (e == hipSuccess) e = fn();
+  if (e == hipSuccess) e = hipEventRecord(b, S->stream);
+  if (e != hipSuccess) {
+    S->free_events.push_back(a);
+    S->free_events.push_back(b);
+    return e;
+  }
   S->pending.push_back({cls, a, b, flops, bytes});
-  return e;
+  return hipSuccess;
 }
 
 #define TRY(expr)                             \
@@ -522,7 +533,9 @@ static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 tp_status tp_slice_forward(tp_stage* S, int l, int r, const void* x, void* y) {
   if (!S || !x || !y || !aligned16(x) || !aligned16(y)) return TP_ERR_INVALID;
   if (l < 0 || r <= l || r > S->L) return TP_ERR_INVALID;
-  if (l != S->cached_len) return TP_ERR_ORDER;
+  // slices arrive in order; once the backward pass of the sequence has begun
+  // (frontier below the cached length) only tp_kv_prefix_reset starts over
+  if (l != S->cached_len || S->bwd_frontier != S->cached_len) return TP_ERR_ORDER;
   tp_status s = forward_impl(S, l, r, x, y);
   if (s != TP_OK) return s;
   S->cached_len = r;
@@ -550,10 +563,13 @@ tp_status tp_profile_slice_cost(tp_stage* S, const int* lens, int n_lens, const 
     if (lens[i] < 1) return TP_ERR_INVALID;
   for (int j = 0; j < n_ctxs; ++j)
     if (ctxs[j] < 0) return TP_ERR_INVALID;
-  hipEvent_t e0, e1, e2;
-  if (hipEventCreate(&e0) != hipSuccess) return TP_ERR_HIP;
-  if (hipEventCreate(&e1) != hipSuccess) return TP_ERR_HIP;
-  if (hipEventCreate(&e2) != hipSuccess) return TP_ERR_HIP;
+  hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr;
+  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess ||
+      hipEventCreate(&e2) != hipSuccess) {
+    for (hipEvent_t e : {e0, e1, e2})
+      if (e) hipEventDestroy(e);
+    return TP_ERR_HIP;
+  }
   const bool was_timing = S->timing;
   S->timing = false;
   S->profiling = true;
@@ -578,20 +594,25 @@ tp_status tp_profile_slice_cost(tp_stage* S, const int* lens, int n_lens, const 
       tb.clear();
       for (int rep = 0; rep < warmup + reps && status == TP_OK; ++rep) {
         S->cached_len = ctx;
-        hipEventRecord(e0, S->stream);
-        status = forward_impl(S, ctx, ctx + len, S->sc.io_a, S->sc.io_b);
-        if (status != TP_OK) break;
-        hipEventRecord(e1, S->stream);
-        status = backward_impl(S, ctx, ctx + len, S->sc.io_a, S->sc.io_b);
-        if (status != TP_OK) break;
-        hipEventRecord(e2, S->stream);
-        if (hipEventSynchronize(e2) != hipSuccess) {
+        if (hipEventRecord(e0, S->stream) != hipSuccess) {
           status = TP_ERR_HIP;
           break;
         }
+        status = forward_impl(S, ctx, ctx + len, S->sc.io_a, S->sc.io_b);
+        if (status != TP_OK) break;
+        if (hipEventRecord(e1, S->stream) != hipSuccess) {
+          status = TP_ERR_HIP;
+          break;
+        }
+        status = backward_impl(S, ctx, ctx + len, S->sc.io_a, S->sc.io_b);
+        if (status != TP_OK) break;
         float f = 0, b = 0;
-        hipEventElapsedTime(&f, e0, e1);
-        hipEventElapsedTime(&b, e1, e2);
+        if (hipEventRecord(e2, S->stream) != hipSuccess || hipEventSynchronize(e2) != hipSuccess ||
+            hipEventElapsedTime(&f, e0, e1) != hipSuccess ||
+            hipEventElapsedTime(&b, e1, e2) != hipSuccess) {
+          status = TP_ERR_HIP;
+          break;
+        }
         if (rep >= warmup) {
           tf.push_back(f);
           tb.push_back(b);
@@ -636,20 +657,29 @@ tp_status tp_stage_enable_kernel_timing(tp_stage* S, int enable) {
 }
 
 int tp_stage_kernel_stats(tp_stage* S, tp_kernel_stat* out, int cap) {
-  if (!S) return 0;
+  if (!S) return -1;
   if (!S->pending.empty()) {
-    if (hipStreamSynchronize(S->stream) != hipSuccess) return 0;
+    bool ok = hipStreamSynchronize(S->stream) == hipSuccess;
     for (auto& p : S->pending) {
       float ms = 0.f;
-      hipEventElapsedTime(&ms, p.a, p.b);
+      if (ok && hipEventElapsedTime(&ms, p.a, p.b) != hipSuccess) ok = false;
+      S->free_events.push_back(p.a);
+      S->free_events.push_back(p.b);
+      if (!ok) continue;
       S->launches[p.cls] += 1;
       S->total_ms[p.cls] += ms;
       S->flops[p.cls] += p.flops;
       S->bytes[p.cls] += p.bytes;
-      S->free_events.push_back(p.a);
-      S->free_events.push_back(p.b);
     }
     S->pending.clear();
+    if (!ok) {
+      // the sums would be wrong: drop them all
+      for (int c = 0; c < K_N; ++c) {
+        S->launches[c] = 0;
+        S->total_ms[c] = S->flops[c] = S->bytes[c] = 0;
+      }
+      return -1;
+    }
   }
   int w = 0;
   for (int c = 0; c < K_N && out && w < cap; ++c) {

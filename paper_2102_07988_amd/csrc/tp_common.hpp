@@ -123,4 +123,10 @@ __device__ inline void st8(bf16* p, const float* x) {
 
 __host__ __device__ inline int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
 
+// A launch reports its status through hipGetLastError(), which also returns an
+// error left behind by any earlier runtime call of the thread (a failed event
+// query, say) that nobody read.  Every launcher calls this before its first
+// launch, so the status it returns belongs to its own launches.
+inline void clear_stale_error() { (void)hipGetLastError(); }
+
 }  // namespace tp

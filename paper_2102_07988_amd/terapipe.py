@@ -284,6 +284,8 @@ class Stage:
     def kernel_stats(self) -> Dict[str, Dict[str, float]]:
         buf = (KernelStat * 16)()
         n = lib.tp_stage_kernel_stats(self._h, buf, 16)
+        if n < 0:
+            raise TerapipeError(TP_ERR_HIP, "tp_stage_kernel_stats")
         return {buf[i].name.decode(): {"launches": buf[i].launches, "total_ms": buf[i].total_ms,
                                        "flops": buf[i].flops, "bytes": buf[i].bytes}
                 for i in range(n)}

@@ -56,3 +56,18 @@ def test_slice_flops_matches_paper_convention_within_rounding():
 def test_slice_flops_small_case_by_hand():
     # n = 2 tokens after c = 3: pairs = 2*3 + 3 = 9; H = 4
     assert slice_flops(2, 3, 4) == 3 * (24 * 2 * 16 + 4 * 4 * 9)
+
+
+@pytest.mark.parametrize("H,L,lens", [(2048, 2048, [256] * 8), (5120, 2048, [256] * 8),
+                                      (12288, 2048, [256] * 8), (12288, 8192, [512] * 16),
+                                      (12288, 2048, [128, 384, 16, 1520])])
+def test_binding_flop_count_equals_oracle(H, L, lens):
+    """The benchmark's headline flop count comes from the binding's copy of the
+    per-slice count; it must equal the oracle's pinned count slice by slice."""
+    from paper_2102_07988_amd import terapipe as tp
+    c = 0
+    for n in lens:
+        assert tp.slice_flops(n, c, H) == slice_flops(n, c, H)
+        c += n
+    assert sum(tp.slice_flops(n, sum(lens[:i]), H) for i, n in enumerate(lens)) == \
+        sequence_flops(lens, H, 1)

@@ -89,6 +89,73 @@ def test_order_errors_leave_state():
     torch.cuda.synchronize()
 
 
+def test_forward_after_backward_is_rejected():
+    """Once a sequence's backward has begun, a forward call is misuse (a slice's
+    backward needs every later slice's forward, Sec. 3.2): TP_ERR_ORDER with the
+    stage unchanged, so the rest of the backward still gives the oracle's
+    gradients; after tp_kv_prefix_reset forward is accepted again."""
+    from paper_2102_07988_amd import terapipe as tp
+    H, heads, L = 64, 4, 32
+    params, x, dy = make_inputs(1, H, L, "fp32", (0, 0, 0), randomize_ln=True)
+    dparams = [{k: v.cuda() for k, v in p.items()} for p in params]
+    st = tp.Stage(dparams, H, heads, L, dtype="fp32")
+    st.reset()
+    xd, dyd = x.cuda(), dy.cuda()
+    y = torch.empty_like(xd)
+    dx = torch.empty_like(dyd)
+    st.forward(0, 16, xd[:16], out=y[:16])
+    st.forward(16, 32, xd[16:], out=y[16:])
+    st.backward(16, 32, dyd[16:], out=dx[16:])
+    for l, r in ((16, 24), (0, 8), (32, 33)):
+        with pytest.raises(tp.TerapipeError) as e:
+            st.forward(l, r, xd[:r - l] if r <= L else xd[:1])
+        assert e.value.status in (tp.TP_ERR_ORDER, tp.TP_ERR_INVALID)
+        if r <= L:
+            assert e.value.status == tp.TP_ERR_ORDER
+    st.backward(0, 16, dyd[:16], out=dx[:16])
+    torch.cuda.synchronize()
+    got = {"y": y.cpu().numpy(), "dx": dx.cpu().numpy(),
+           "grads": [{k: v.cpu().numpy() for k, v in g.items()} for g in st.grads]}
+    ref = run_oracle(params, x, dy, H, heads, L, [16, 16])
+    compare(got, ref, TOL["fp32"], "forward after backward rejected")
+    st.reset()
+    st.forward(0, 8, xd[:8])
+    torch.cuda.synchronize()
+
+
+def test_stale_runtime_error_is_not_blamed_on_the_next_call():
+    """A failed HIP runtime call made outside the library (here: the elapsed time
+    of two events that were never recorded, a host-side error, no GPU fault)
+    leaves an error in the thread's last-error slot.  The library's next calls
+    must report their own status: reset and a slice forward return TP_OK."""
+    import ctypes
+    from paper_2102_07988_amd import terapipe as tp
+    H, heads, L = 64, 4, 32
+    params, x, _ = make_inputs(1, H, L, "bf16", (0, 0, 0))
+    dparams = [{k: v.cuda() for k, v in p.items()} for p in params]
+    st = tp.Stage(dparams, H, heads, L, dtype="bf16")
+    torch.cuda.synchronize()
+    hip = ctypes.CDLL("libamdhip64.so")
+    e0, e1 = ctypes.c_void_p(), ctypes.c_void_p()
+    assert hip.hipEventCreate(ctypes.byref(e0)) == 0
+    assert hip.hipEventCreate(ctypes.byref(e1)) == 0
+    ms = ctypes.c_float()
+    rc = hip.hipEventElapsedTime(ctypes.byref(ms), e0, e1)
+    print(f"hipEventElapsedTime on unrecorded events: {rc}", flush=True)
+    assert rc != 0
+    assert tp.lib.tp_kv_prefix_reset(st.handle) == tp.TP_OK
+    xd = x.cuda()
+    y = torch.empty_like(xd)
+    # and once more with the error planted again right before a slice forward
+    assert hip.hipEventElapsedTime(ctypes.byref(ms), e0, e1) != 0
+    assert tp.lib.tp_slice_forward(st.handle, 0, L, ctypes.c_void_p(xd.data_ptr()),
+                                   ctypes.c_void_p(y.data_ptr())) == tp.TP_OK
+    torch.cuda.synchronize()
+    assert torch.isfinite(y.float()).all()
+    hip.hipEventDestroy(e0)
+    hip.hipEventDestroy(e1)
+
+
 @pytest.mark.parametrize("H,heads", [(256, 2), (256, 4)])  # d = 128, 64
 @pytest.mark.parametrize("wgrad", ["per_slice", "deferred"])
 def test_matrix_core_attention_ragged(H, heads, wgrad):
