@@ -27,6 +27,20 @@
  *    only.  Matrices are row-major; weight matrices are [out][in].
  *  - Activations and parameters use the stage dtype (bf16 or fp32); gradients
  *    are always fp32 and are ACCUMULATED (+=): the caller zeroes them.
+ *  - Precision of a bf16 stage whose head width is 64 or 128: matrix products
+ *    take bf16 operands with fp32 accumulation, except that (1) the residual
+ *    stream inside the stage (the input of every layer but the first, and x1)
+ *    is kept in fp32, and (2) the query/key/value product and the attention
+ *    scores run on fp16 operands: the LN1 output, a copy of W_qkv converted to
+ *    fp16 by tp_kv_prefix_reset (so W_qkv must not change during a sequence,
+ *    and its entries must lie within the fp16 range), q, k and the forward's
+ *    v; the forward's softmax weights and the backward's dS are fp16 where
+ *    they meet those operands.  With bf16 there, the rounding of the LN1 output
+ *    and of q and k is amplified by sharp softmax rows (e.g. logits of standard
+ *    deviation ~5 at hidden size 12288 with N(0, 0.02) weights) to several
+ *    percent of relative error in the gradients; fp16 keeps 3 more mantissa
+ *    bits at the same matrix-core rate.  Gradient-side operands stay bf16.
+ *    Other bf16 stages (head widths 16, 32) use bf16 throughout.
  *  - Calls are asynchronous on the stage's stream unless stated otherwise; a
  *    HIP launch failure is reported as TP_ERR_HIP.  Argument and ordering
  *    errors are detected on the host before anything is enqueued and leave
@@ -120,7 +134,9 @@ tp_status tp_stage_init(const tp_stage_config *cfg, const tp_layer_ptrs *params,
 void tp_stage_destroy(tp_stage *stage);
 
 /* Start a new sequence: no cached tokens, backward frontier 0, and the fp32
- * dK/dV buffer zeroed (enqueued on the stream; a fill kernel, no memset node).
+ * dK/dV buffer zeroed (enqueued on the stream; a fill kernel, no memset node);
+ * on the mixed-precision path (see Conventions) also the fp16 copy of every
+ * layer's W_qkv taken.
  * This is the empty prefix state of Eq. 2: the keys and values of positions
  * before the first slice, which every later slice's attention sums over,
  * start out empty (Sec. 3.2: the cell keeps them from slice to slice).

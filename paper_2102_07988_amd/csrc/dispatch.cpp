@@ -19,6 +19,9 @@ hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s) {
     e = gemm_mfma_bf16(a, s);
     if (e != hipErrorNotSupported) return e;
   }
+  // fp16 operands have no generic kernel (the stage only asks for them where
+  // the matrix-core kernels apply)
+  if (a.in_f16) return hipErrorNotSupported;
   return gemm_generic(dtype, a, s);
 }
 
@@ -31,6 +34,7 @@ hipError_t attn_fwd(int dtype, const AttnArgs& a, hipStream_t s) {
     const hipError_t e = attn_fwd_mfma_bf16(a, s);
     if (e != hipErrorNotSupported) return e;
   }
+  if (a.f16) return hipErrorNotSupported;
   return attn_fwd_generic(dtype, a, s);
 }
 
@@ -40,6 +44,7 @@ hipError_t attn_bwd(int dtype, const AttnArgs& a, hipStream_t s) {
     const hipError_t e = attn_bwd_mfma_bf16(a, s);
     if (e != hipErrorNotSupported) return e;
   }
+  if (a.f16) return hipErrorNotSupported;
   return attn_bwd_generic(dtype, a, s);
 }
 

@@ -38,9 +38,20 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+
 __device__ inline f32x16_t mfma(u32x4 a, u32x4 b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
                                                  __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+// fp16 operands (F16) or bf16
+template <bool F16>
+__device__ inline f32x16_t mfma_t(u32x4 a, u32x4 b, f32x16_t c) {
+  if constexpr (F16)
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, a),
+                                                  __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
+  else
+    return mfma(a, b, c);
 }
 
 __device__ inline f32x16_t zero16() {
@@ -92,6 +103,27 @@ __device__ inline u32x4 acc_half_bf16(const f32x16_t& x, int ks) {
   u.z = pack_bf16x2(x[o + 4], x[o + 5]);
   u.w = pack_bf16x2(x[o + 6], x[o + 7]);
   return u;
+}
+// Two fp32 values as round-to-nearest-even fp16 (lo in the low half).
+__device__ inline uint32_t pack_f16x2(float lo, float hi) {
+  typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, f16x2_t));
+}
+// 8 accumulator values as an fp16 (F16) or bf16 operand.
+template <bool F16>
+__device__ inline u32x4 acc_half(const f32x16_t& x, int ks) {
+  if constexpr (F16) {
+    u32x4 u;
+    const int o = 8 * ks;
+    u.x = pack_f16x2(x[o + 0], x[o + 1]);
+    u.y = pack_f16x2(x[o + 2], x[o + 3]);
+    u.z = pack_f16x2(x[o + 4], x[o + 5]);
+    u.w = pack_f16x2(x[o + 6], x[o + 7]);
+    return u;
+  } else {
+    return acc_half_bf16(x, ks);
+  }
 }
 
 // Tile of rows x D bf16 in LDS, rows of 2D bytes whose 16-byte chunks are
@@ -171,7 +203,8 @@ struct Tile {
 // other's matrix products
 // SPLIT: this block takes only split blockIdx.z % nsplit of the keys and
 // leaves the unnormalised output with its running maximum and sum.
-template <int D, int NW, bool SPLIT>
+// F16: q, k and v are fp16 (scores and P V on fp16 operands), else bf16.
+template <int D, int NW, bool SPLIT, bool F16>
 __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a0) {
   const AttnArgs a = attn_seq_view<uint16_t>(a0);
   const int zsp = SPLIT ? blockIdx.z % a.nsplit : 0;
@@ -243,9 +276,9 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a0) {
           lgkm_wait(kf[0]);
 #pragma unroll
           for (int kk = 1; kk < KS; ++kk) lgkm_tie(kf[kk]);
-          s = mfma(kf[0], qf[0], zero16());
+          s = mfma_t<F16>(kf[0], qf[0], zero16());
 #pragma unroll
-          for (int kk = 1; kk < KS; ++kk) s = mfma(kf[kk], qf[kk], s);
+          for (int kk = 1; kk < KS; ++kk) s = mfma_t<F16>(kf[kk], qf[kk], s);
         }
         // keys of a sub-block that ends at or before the wave's first query
         // need no mask (all are <= every query of the wave and < r)
@@ -292,7 +325,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a0) {
         if (kbase + 32 * sb >= kend_w) break;
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-          const u32x4 pb = acc_half_bf16(p[sb], ks);
+          const u32x4 pb = acc_half<F16>(p[sb], ks);
           u32x4 vf[JB];
 #pragma unroll
           for (int j = 0; j < JB; ++j) vf[j] = T::col8(Vt, 32 * sb + 16 * ks, 32 * j, lane);
@@ -300,7 +333,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_fwd_mfma(AttnArgs a0) {
 #pragma unroll
           for (int j = 1; j < JB; ++j) lgkm_tie(vf[j]);
 #pragma unroll
-          for (int j = 0; j < JB; ++j) o[j] = mfma(vf[j], pb, o[j]);
+          for (int j = 0; j < JB; ++j) o[j] = mfma_t<F16>(vf[j], pb, o[j]);
         }
       }
     }
@@ -361,7 +394,9 @@ __global__ __launch_bounds__(256) void attn_bwd_rowdot(AttnArgs a0) {
 // recomputes S once more than a kernel forming both would.
 // ST query tiles form the LDS ring: tile qb + ST - 1 is requested while tile
 // qb is multiplied.
-template <int D, int NW, int MODE, int ST>
+// F16: q and k are fp16 (scores on fp16 operands; the dK kernel's dS product
+// on fp16 dS); v and the gradients stay bf16.
+template <int D, int NW, int MODE, int ST, bool F16>
 __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dkdv_mfma(AttnArgs a0) {
   static_assert(MODE == 1 || MODE == 2, "dV (1) or dK (2)");
   const AttnArgs a = attn_seq_view<uint16_t>(a0);
@@ -446,7 +481,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dkdv_mfma(AttnArgs a0) {
 #pragma unroll
         for (int b = 0; b < 4; ++b) lgkm_tie(lq[b]);
 #pragma unroll
-        for (int kk = 0; kk < KS; ++kk) s = mfma(qa[kk], kf[kk], s);
+        for (int kk = 0; kk < KS; ++kk) s = mfma_t<F16>(qa[kk], kf[kk], s);
       }
       // s[v]: query row qi = 8 (v / 4) + 4 G + v % 4 of the block, key s_me.
       // P first, so the lse values are dead before the dP product.
@@ -515,7 +550,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dkdv_mfma(AttnArgs a0) {
           for (int j = 0; j < JB; ++j) dv[j] = mfma(pb, ob[j], dv[j]);
         }
         if constexpr (DO_K) {
-          const u32x4 db = acc_half_bf16(ds, ks);
+          const u32x4 db = acc_half<F16>(ds, ks);
           u32x4 qb2[JB];
 #pragma unroll
           for (int j = 0; j < JB; ++j) qb2[j] = T::col8(Qt, 16 * ks, 32 * j, lane);
@@ -523,7 +558,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dkdv_mfma(AttnArgs a0) {
 #pragma unroll
           for (int j = 1; j < JB; ++j) lgkm_tie(qb2[j]);
 #pragma unroll
-          for (int j = 0; j < JB; ++j) dk[j] = mfma(db, qb2[j], dk[j]);
+          for (int j = 0; j < JB; ++j) dk[j] = mfma_t<F16>(db, qb2[j], dk[j]);
         }
       }
     }
@@ -584,7 +619,8 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dkdv_mfma(AttnArgs a0) {
 
 // SPLIT: this block takes only split blockIdx.z % nsplit of the keys and
 // leaves its unscaled fp32 dQ partial.
-template <int D, int NW, bool SPLIT>
+// F16: q and k are fp16 (scores and the dS K product on fp16 operands).
+template <int D, int NW, bool SPLIT, bool F16>
 __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a0) {
   const AttnArgs a = attn_seq_view<uint16_t>(a0);
   const int zsp = SPLIT ? blockIdx.z % a.nsplit : 0;
@@ -653,7 +689,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a0) {
 #pragma unroll
         for (int kk = 1; kk < KS; ++kk) lgkm_tie(ka[kk]);
 #pragma unroll
-        for (int kk = 0; kk < KS; ++kk) s = mfma(ka[kk], qf[kk], s);
+        for (int kk = 0; kk < KS; ++kk) s = mfma_t<F16>(ka[kk], qf[kk], s);
       }
       {
         u32x4 va[KS];
@@ -683,7 +719,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a0) {
       }
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-        const u32x4 db = acc_half_bf16(ds, ks);
+        const u32x4 db = acc_half<F16>(ds, ks);
         u32x4 kt[JB];
 #pragma unroll
         for (int j = 0; j < JB; ++j) kt[j] = T::col8(Kt, 32 * sb + 16 * ks, 32 * j, lane);
@@ -691,7 +727,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a0) {
 #pragma unroll
         for (int j = 1; j < JB; ++j) lgkm_tie(kt[j]);
 #pragma unroll
-        for (int j = 0; j < JB; ++j) dq[j] = mfma(kt[j], db, dq[j]);
+        for (int j = 0; j < JB; ++j) dq[j] = mfma_t<F16>(kt[j], db, dq[j]);
       }
     }
   }
@@ -804,21 +840,22 @@ hipError_t set_lds(K* fn, size_t bytes) {
                              (int)bytes);
 }
 
-template <int D>
+template <int D, bool F16>
 hipError_t fwd_d(const AttnArgs& a, hipStream_t s) {
   const int n = a.r - a.l;
   constexpr size_t lds = 2 * 2 * 64 * D * 2;
   AttnArgs b = a;
   plan_split(b, true);
   if (b.nsplit == 1) {
-    hipError_t e = set_lds(attn_fwd_mfma<D, NWF, false>, lds);
+    hipError_t e = set_lds(attn_fwd_mfma<D, NWF, false, F16>, lds);
     if (e != hipSuccess) return e;
-    attn_fwd_mfma<D, NWF, false><<<dim3(cdiv(n, 32 * NWF), a.heads, a.bs), 64 * NWF, lds, s>>>(a);
+    attn_fwd_mfma<D, NWF, false, F16>
+        <<<dim3(cdiv(n, 32 * NWF), a.heads, a.bs), 64 * NWF, lds, s>>>(a);
     return hipGetLastError();
   }
-  hipError_t e = set_lds(attn_fwd_mfma<D, NWF, true>, lds);
+  hipError_t e = set_lds(attn_fwd_mfma<D, NWF, true, F16>, lds);
   if (e != hipSuccess) return e;
-  attn_fwd_mfma<D, NWF, true>
+  attn_fwd_mfma<D, NWF, true, F16>
       <<<dim3(cdiv(n, 32 * NWF), a.heads, a.bs * b.nsplit), 64 * NWF, lds, s>>>(b);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -826,10 +863,31 @@ hipError_t fwd_d(const AttnArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int D>
-hipError_t dq_d(const AttnArgs& a, hipStream_t s);
+template <int D, bool F16>
+hipError_t dq_d(const AttnArgs& a, hipStream_t s) {
+  const int n = a.r - a.l;
+  hipError_t e;
+  constexpr size_t lds_q = 2 * 2 * 64 * D * 2;
+  AttnArgs b = a;
+  plan_split(b, false);
+  if (b.nsplit == 1) {
+    e = set_lds(attn_bwd_dq_mfma<D, NWF, false, F16>, lds_q);
+    if (e != hipSuccess) return e;
+    attn_bwd_dq_mfma<D, NWF, false, F16>
+        <<<dim3(cdiv(n, 32 * NWF), a.heads, a.bs), 64 * NWF, lds_q, s>>>(a);
+    return hipGetLastError();
+  }
+  e = set_lds(attn_bwd_dq_mfma<D, NWF, true, F16>, lds_q);
+  if (e != hipSuccess) return e;
+  attn_bwd_dq_mfma<D, NWF, true, F16>
+      <<<dim3(cdiv(n, 32 * NWF), a.heads, a.bs * b.nsplit), 64 * NWF, lds_q, s>>>(b);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  attn_dq_combine<<<cdiv((long)n * a.bs * (a.H / 8), 256), 256, 0, s>>>(b);
+  return hipGetLastError();
+}
 
-template <int D>
+template <int D, bool F16>
 hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
   const int n = a.r - a.l;
   attn_bwd_rowdot<D><<<dim3(cdiv((long)n * a.heads, 4), 1, a.bs), 256, 0, s>>>(a);
@@ -848,55 +906,33 @@ hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
     // four-wave dK blocks over two-tile rings, so more blocks share the CUs
     constexpr size_t lds_v2 = 2 * (2 * 32 * D + 2 * 128) * 2;
     constexpr size_t lds_k4 = 2 * (2 * 32 * D + 4 * 128) * 2 + 32 * 4 * D * 2;
-    e = set_lds(attn_bwd_dkdv_mfma<D, 2, 1, 2>, lds_v2);
+    e = set_lds(attn_bwd_dkdv_mfma<D, 2, 1, 2, F16>, lds_v2);
     if (e != hipSuccess) return e;
-    attn_bwd_dkdv_mfma<D, 2, 1, 2><<<dim3(cdiv(a.r, 64), a.heads, a.bs), 128, lds_v2, s>>>(a);
+    attn_bwd_dkdv_mfma<D, 2, 1, 2, F16>
+        <<<dim3(cdiv(a.r, 64), a.heads, a.bs), 128, lds_v2, s>>>(a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    e = set_lds(attn_bwd_dkdv_mfma<D, 4, 2, 2>, lds_k4);
+    e = set_lds(attn_bwd_dkdv_mfma<D, 4, 2, 2, F16>, lds_k4);
     if (e != hipSuccess) return e;
-    attn_bwd_dkdv_mfma<D, 4, 2, 2><<<dim3(cdiv(a.r, 128), a.heads, a.bs), 256, lds_k4, s>>>(a);
+    attn_bwd_dkdv_mfma<D, 4, 2, 2, F16>
+        <<<dim3(cdiv(a.r, 128), a.heads, a.bs), 256, lds_k4, s>>>(a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    return dq_d<D>(a, s);
+    return dq_d<D, F16>(a, s);
   }
-  e = set_lds(attn_bwd_dkdv_mfma<D, NWF, 1, STA>, lds_a);
+  e = set_lds(attn_bwd_dkdv_mfma<D, NWF, 1, STA, F16>, lds_a);
   if (e != hipSuccess) return e;
-  attn_bwd_dkdv_mfma<D, NWF, 1, STA>
+  attn_bwd_dkdv_mfma<D, NWF, 1, STA, F16>
       <<<dim3(cdiv(a.r, 32 * NWF), a.heads, a.bs), 64 * NWF, lds_a, s>>>(a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  e = set_lds(attn_bwd_dkdv_mfma<D, NWK, 2, STK>, lds_k);
+  e = set_lds(attn_bwd_dkdv_mfma<D, NWK, 2, STK, F16>, lds_k);
   if (e != hipSuccess) return e;
-  attn_bwd_dkdv_mfma<D, NWK, 2, STK>
+  attn_bwd_dkdv_mfma<D, NWK, 2, STK, F16>
       <<<dim3(cdiv(a.r, 32 * NWK), a.heads, a.bs), 64 * NWK, lds_k, s>>>(a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return dq_d<D>(a, s);
-}
-
-template <int D>
-hipError_t dq_d(const AttnArgs& a, hipStream_t s) {
-  const int n = a.r - a.l;
-  hipError_t e;
-  constexpr size_t lds_q = 2 * 2 * 64 * D * 2;
-  AttnArgs b = a;
-  plan_split(b, false);
-  if (b.nsplit == 1) {
-    e = set_lds(attn_bwd_dq_mfma<D, NWF, false>, lds_q);
-    if (e != hipSuccess) return e;
-    attn_bwd_dq_mfma<D, NWF, false>
-        <<<dim3(cdiv(n, 32 * NWF), a.heads, a.bs), 64 * NWF, lds_q, s>>>(a);
-    return hipGetLastError();
-  }
-  e = set_lds(attn_bwd_dq_mfma<D, NWF, true>, lds_q);
-  if (e != hipSuccess) return e;
-  attn_bwd_dq_mfma<D, NWF, true>
-      <<<dim3(cdiv(n, 32 * NWF), a.heads, a.bs * b.nsplit), 64 * NWF, lds_q, s>>>(b);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  attn_dq_combine<<<cdiv((long)n * a.bs * (a.H / 8), 256), 256, 0, s>>>(b);
-  return hipGetLastError();
+  return dq_d<D, F16>(a, s);
 }
 
 inline bool al16(const void* p) { return ((uintptr_t)p & 15) == 0; }
@@ -910,13 +946,15 @@ bool covered(const AttnArgs& a) {
 
 hipError_t attn_fwd_mfma_bf16(const AttnArgs& a, hipStream_t s) {
   if (!covered(a) || !al16(a.o)) return hipErrorNotSupported;
-  return a.d == 128 ? fwd_d<128>(a, s) : fwd_d<64>(a, s);
+  if (a.f16) return a.d == 128 ? fwd_d<128, true>(a, s) : fwd_d<64, true>(a, s);
+  return a.d == 128 ? fwd_d<128, false>(a, s) : fwd_d<64, false>(a, s);
 }
 
 hipError_t attn_bwd_mfma_bf16(const AttnArgs& a, hipStream_t s) {
   if (!covered(a) || !al16(a.dout) || !al16(a.dq) || (a.ld_dq % 8) || (a.dq_seq % 8))
     return hipErrorNotSupported;
-  return a.d == 128 ? bwd_d<128>(a, s) : bwd_d<64>(a, s);
+  if (a.f16) return a.d == 128 ? bwd_d<128, true>(a, s) : bwd_d<64, true>(a, s);
+  return a.d == 128 ? bwd_d<128, false>(a, s) : bwd_d<64, false>(a, s);
 }
 
 }  // namespace tp

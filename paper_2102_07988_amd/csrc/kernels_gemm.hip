@@ -13,6 +13,7 @@
 // registers before it is written.  The next k-tile is fetched into registers
 // while the current one is multiplied.
 #include "tp_common.hpp"
+#include "tp_epilogue.hpp"
 #include "tp_kernels.hpp"
 
 #include <algorithm>
@@ -22,6 +23,7 @@ namespace tp {
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int BK = 64;
@@ -33,35 +35,6 @@ constexpr int BK = 64;
 // spread over all chunks.
 __device__ inline int swz(int r) { return (r ^ (r >> 3)) & 7; }
 __device__ inline int lds_off(int r, int k) { return r * BK + ((((k >> 3) ^ swz(r))) << 3) + (k & 7); }
-
-template <typename T, int EPI>
-__device__ inline void epi_store(const GemmArgs& a, int m, int n, float acc) {
-  if constexpr (EPI == EPI_ACC_F32) {
-    float* C = (float*)a.C + (long)m * a.ldc + n;
-    *C += acc;
-  } else if constexpr (EPI == EPI_DGELU) {
-    const float z = ld((const T*)a.R + (long)m * a.ldr + n);
-    st((T*)a.C + (long)m * a.ldc + n, acc * gelu_tanh_grad(z));
-  } else {
-    const float v = acc + (a.bias ? ld((const T*)a.bias + n) : 0.f);
-    if constexpr (EPI == EPI_STORE) {
-      st((T*)a.C + (long)m * a.ldc + n, v);
-    } else if constexpr (EPI == EPI_RESID) {
-      st((T*)a.C + (long)m * a.ldc + n, v + ld((const T*)a.R + (long)m * a.ldr + n));
-    } else if constexpr (EPI == EPI_GELU) {
-      st((T*)a.C + (long)m * a.ldc + n, v);
-      st((T*)a.C2 + (long)m * a.ldc2 + n, gelu_tanh(v));
-    } else if constexpr (EPI == EPI_QKV) {
-      const int H = a.H;
-      if (n < H)
-        st((T*)a.q + (long)m * H + n, v);
-      else if (n < 2 * H)
-        st((T*)a.k + (long)m * H + (n - H), v);
-      else
-        st((T*)a.v + (long)m * H + (n - 2 * H), v);
-    }
-  }
-}
 
 __device__ inline uint4 pack8(const uint16_t* t) {
   return make_uint4(t[0] | (uint32_t)t[1] << 16, t[2] | (uint32_t)t[3] << 16,
@@ -163,7 +136,8 @@ struct TileSel<R, NTH, false> {
   using type = TileMC<R, NTH>;
 };
 
-template <int BM, int BN, int WGM, int WGN, bool A_KC, bool B_KC, int EPI, bool SPLIT>
+// F16: both operands are fp16 (the mixed-precision query/key/value product).
+template <int BM, int BN, int WGM, int WGN, bool A_KC, bool B_KC, int EPI, bool SPLIT, bool F16>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_mfma_kernel(GemmArgs a) {
   constexpr int NTH = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
@@ -219,8 +193,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_mfma_kernel(GemmArgs a) {
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < FN; ++j) {
+          if constexpr (F16)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, af[i]),
+                                                               __builtin_bit_cast(f16x8_t, bfr[j]),
+                                                               acc[i][j], 0, 0, 0);
+          else
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        }
     }
     if (kt + 1 < nk) {
       __syncthreads();
@@ -244,7 +224,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_mfma_kernel(GemmArgs a) {
           if constexpr (SPLIT)
             part[(long)m * a.N + n] = acc[i][j][v];
           else
-            epi_store<bf16, EPI>(a, m, n, acc[i][j][v]);
+            epi1<bf16, EPI>(a, m, n, acc[i][j][v]);
         }
       }
 }
@@ -256,7 +236,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
   for (long e = (long)blockIdx.x * 256 + threadIdx.x; e < tot; e += (long)gridDim.x * 256) {
     float s = 0.f;
     for (int z = 0; z < a.splits; ++z) s += a.ws[(long)z * tot + e];
-    epi_store<bf16, EPI>(a, (int)(e / a.N), (int)(e % a.N), s);
+    epi1<bf16, EPI>(a, (int)(e / a.N), (int)(e % a.N), s);
   }
 }
 
@@ -277,46 +257,7 @@ __global__ __launch_bounds__(256) void splitk_reduce8_kernel(GemmArgs a) {
       s[0] += u.x, s[1] += u.y, s[2] += u.z, s[3] += u.w;
       s[4] += w.x, s[5] += w.y, s[6] += w.z, s[7] += w.w;
     }
-    if constexpr (EPI == EPI_ACC_F32) {
-      float4* c = (float4*)((float*)a.C + (long)m * a.ldc + n);
-      float4 u = c[0], w = c[1];
-      u.x += s[0], u.y += s[1], u.z += s[2], u.w += s[3];
-      w.x += s[4], w.y += s[5], w.z += s[6], w.w += s[7];
-      c[0] = u, c[1] = w;
-    } else if constexpr (EPI == EPI_DGELU) {
-      float z[8];
-      ld8((const bf16*)a.R + (long)m * a.ldr + n, z);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) s[i] *= gelu_tanh_grad(z[i]);
-      st8((bf16*)a.C + (long)m * a.ldc + n, s);
-    } else {
-      if (a.bias) {
-        float b[8];
-        ld8((const bf16*)a.bias + n, b);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) s[i] += b[i];
-      }
-      if constexpr (EPI == EPI_STORE) {
-        st8((bf16*)a.C + (long)m * a.ldc + n, s);
-      } else if constexpr (EPI == EPI_RESID) {
-        float r[8];
-        ld8((const bf16*)a.R + (long)m * a.ldr + n, r);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) s[i] += r[i];
-        st8((bf16*)a.C + (long)m * a.ldc + n, s);
-      } else if constexpr (EPI == EPI_GELU) {
-        st8((bf16*)a.C + (long)m * a.ldc + n, s);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) s[i] = gelu_tanh(s[i]);
-        st8((bf16*)a.C2 + (long)m * a.ldc2 + n, s);
-      } else if constexpr (EPI == EPI_QKV) {
-        const int H = a.H;
-        bf16* dst = n < H ? (bf16*)a.q + (long)m * H + n
-                  : n < 2 * H ? (bf16*)a.k + (long)m * H + (n - H)
-                              : (bf16*)a.v + (long)m * H + (n - 2 * H);
-        st8(dst, s);
-      }
-    }
+    epi8<EPI>(a, m, n, s);
   }
 }
 
@@ -324,12 +265,26 @@ template <int BM, int BN, int WGM, int WGN, bool A_KC, bool B_KC, bool SPLIT>
 hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
   dim3 grid(cdiv(a.N, BN), cdiv(a.M, BM), SPLIT ? a.splits : 1);
   constexpr int NTH = 64 * WGM * WGN;
+  if (a.in_f16) {
+    // fp16 operands: the query/key/value product (k-contiguous operands only)
+    if constexpr (A_KC && B_KC) {
+      if (SPLIT)
+        gemm_mfma_kernel<BM, BN, WGM, WGN, true, true, EPI_STORE, true, true><<<grid, NTH, 0, s>>>(a);
+      else if (a.epi == EPI_QKV)
+        gemm_mfma_kernel<BM, BN, WGM, WGN, true, true, EPI_QKV, false, true><<<grid, NTH, 0, s>>>(a);
+      else
+        return hipErrorNotSupported;
+      return hipGetLastError();
+    } else {
+      return hipErrorNotSupported;
+    }
+  }
   if constexpr (SPLIT) {
-    gemm_mfma_kernel<BM, BN, WGM, WGN, A_KC, B_KC, EPI_STORE, true><<<grid, NTH, 0, s>>>(a);
+    gemm_mfma_kernel<BM, BN, WGM, WGN, A_KC, B_KC, EPI_STORE, true, false><<<grid, NTH, 0, s>>>(a);
   } else {
     switch (a.epi) {
 #define TP_CASE(E) \
-  case E: gemm_mfma_kernel<BM, BN, WGM, WGN, A_KC, B_KC, E, false><<<grid, NTH, 0, s>>>(a); break;
+  case E: gemm_mfma_kernel<BM, BN, WGM, WGN, A_KC, B_KC, E, false, false><<<grid, NTH, 0, s>>>(a); break;
       TP_CASE(EPI_STORE)
       TP_CASE(EPI_QKV)
       TP_CASE(EPI_RESID)
@@ -420,6 +375,7 @@ bool vec8_ok(const GemmArgs& a) {
   if ((a.epi == EPI_RESID || a.epi == EPI_DGELU) && (!al(a.R) || a.ldr % 8)) return false;
   if (a.epi == EPI_GELU && (!al(a.C2) || a.ldc2 % 8)) return false;
   if (a.epi == EPI_QKV && (a.H % 8 || !al(a.q) || !al(a.k) || !al(a.v))) return false;
+  if (a.epi == EPI_QKV && a.qkv_f16 && !al(a.vb)) return false;
   return true;
 }
 

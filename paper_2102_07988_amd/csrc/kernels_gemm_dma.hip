@@ -23,6 +23,7 @@
 #include <type_traits>
 
 #include "tp_common.hpp"
+#include "tp_epilogue.hpp"
 #include "tp_kernels.hpp"
 
 namespace tp {
@@ -32,6 +33,7 @@ hipError_t gemm_splitk_reduce(const GemmArgs& a, hipStream_t s);
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -59,75 +61,6 @@ __device__ inline int swz_mc(int k) {
   static_assert(R % 128 == 0 || R == 192, "transposing-read swizzle needs R = 128 j or 192");
   if constexpr (R == 192) return ((k >> 1) & 1) << 2;
   else return (k & 3) << 2;
-}
-
-template <typename T, int EPI>
-__device__ inline void epi_store(const GemmArgs& a, int m, int n, float acc) {
-  if constexpr (EPI == EPI_ACC_F32) {
-    float* C = (float*)a.C + (long)m * a.ldc + n;
-    *C += acc;
-  } else if constexpr (EPI == EPI_DGELU) {
-    const float z = ld((const T*)a.R + (long)m * a.ldr + n);
-    st((T*)a.C + (long)m * a.ldc + n, acc * gelu_tanh_grad(z));
-  } else {
-    const float v = acc + (a.bias ? ld((const T*)a.bias + n) : 0.f);
-    if constexpr (EPI == EPI_STORE) {
-      st((T*)a.C + (long)m * a.ldc + n, v);
-    } else if constexpr (EPI == EPI_RESID) {
-      st((T*)a.C + (long)m * a.ldc + n, v + ld((const T*)a.R + (long)m * a.ldr + n));
-    } else if constexpr (EPI == EPI_GELU) {
-      st((T*)a.C + (long)m * a.ldc + n, v);
-      st((T*)a.C2 + (long)m * a.ldc2 + n, gelu_tanh(v));
-    } else if constexpr (EPI == EPI_QKV) {
-      const int H = a.H;
-      if (n < H)
-        st((T*)a.q + (long)m * H + n, v);
-      else if (n < 2 * H)
-        st((T*)a.k + (long)m * H + (n - H), v);
-      else
-        st((T*)a.v + (long)m * H + (n - 2 * H), v);
-    }
-  }
-}
-
-// The bf16 epilogues for 8 consecutive columns n .. n+7 of row m (16-byte
-// accesses; the launcher checked sizes and alignment).
-template <int EPI>
-__device__ inline void epi_store8(const GemmArgs& a, int m, int n, float* x) {
-  if constexpr (EPI == EPI_DGELU) {
-    float z[8];
-    ld8((const bf16*)a.R + (long)m * a.ldr + n, z);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] *= gelu_tanh_grad(z[i]);
-    st8((bf16*)a.C + (long)m * a.ldc + n, x);
-  } else {
-    if (a.bias) {
-      float b[8];
-      ld8((const bf16*)a.bias + n, b);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) x[i] += b[i];
-    }
-    if constexpr (EPI == EPI_STORE) {
-      st8((bf16*)a.C + (long)m * a.ldc + n, x);
-    } else if constexpr (EPI == EPI_RESID) {
-      float r[8];
-      ld8((const bf16*)a.R + (long)m * a.ldr + n, r);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) x[i] += r[i];
-      st8((bf16*)a.C + (long)m * a.ldc + n, x);
-    } else if constexpr (EPI == EPI_GELU) {
-      st8((bf16*)a.C + (long)m * a.ldc + n, x);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) x[i] = gelu_tanh(x[i]);
-      st8((bf16*)a.C2 + (long)m * a.ldc2 + n, x);
-    } else if constexpr (EPI == EPI_QKV) {
-      const int H = a.H;
-      bf16* dst = n < H       ? (bf16*)a.q + (long)m * H + n
-                  : n < 2 * H ? (bf16*)a.k + (long)m * H + (n - H)
-                              : (bf16*)a.v + (long)m * H + (n - 2 * H);
-      st8(dst, x);
-    }
-  }
 }
 
 __device__ inline void dma16(const uint16_t* g, uint16_t* lds_wave_base) {
@@ -262,8 +195,10 @@ struct TileWalk {
 // (A, B) stages.  SB == STAGES + 1 == 3 ("B leads"): separate rings, the B
 // operand (the weights of a slice-shaped product, streamed from HBM) one
 // k-tile further ahead than A (activations, L2-resident).
+// F16: both operands are fp16 (the mixed-precision query/key/value product),
+// otherwise bf16.
 template <int BM, int BN, int BK, int WGM, int WGN, bool A_KC, bool B_KC, int EPI, bool SPLIT,
-          int STAGES, int SB>
+          int STAGES, int SB, bool F16>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
   constexpr int NTH = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
@@ -400,9 +335,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
   constexpr int NR = FM + FN, NM = FM * FN;
   auto mfma_at = [&](int buf, int t) {
     const int i = t / FN, j = t % FN;
-    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-        __builtin_bit_cast(bf16x8_t, fa[buf][i]), __builtin_bit_cast(bf16x8_t, fb[buf][j]),
-        acc[i][j], 0, 0, 0);
+    if constexpr (F16)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+          __builtin_bit_cast(f16x8_t, fa[buf][i]), __builtin_bit_cast(f16x8_t, fb[buf][j]),
+          acc[i][j], 0, 0, 0);
+    else
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+          __builtin_bit_cast(bf16x8_t, fa[buf][i]), __builtin_bit_cast(bf16x8_t, fb[buf][j]),
+          acc[i][j], 0, 0, 0);
   };
   auto read_at = [&](int buf, uint32_t ta, uint32_t tb, int k0, int r) {
     if (r < FM) fa[buf][r] = frag_read<BM, BK, A_KC>(ta, wm0 + 32 * r, k0, lane);
@@ -552,14 +492,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
           const float4 w = *(const float4*)(patch + r * 36 + ec + 4);
           float x[8] = {u.x, u.y, u.z, u.w, w.x, w.y, w.z, w.w};
           const int m = m0 + wm0 + 32 * i + r, n = n0 + wn0 + 32 * j + ec;
-          if (m < a.M && n < a.N) epi_store8<EPI>(a, m, n, x);
+          if (m < a.M && n < a.N) epi8<EPI>(a, m, n, x);
         }
       }
   }
 }
 
 template <int BM, int BN, int BK, int WGM, int WGN, bool A_KC, bool B_KC, int STAGES, int SB,
-          bool SPLIT>
+          bool SPLIT, bool F16>
 hipError_t launch_dma(const GemmArgs& a, hipStream_t s) {
   constexpr int NTH = 64 * WGM * WGN;
   constexpr size_t lds = ((size_t)STAGES * BM + (size_t)SB * BN) * BK * 2;
@@ -576,7 +516,7 @@ hipError_t launch_dma(const GemmArgs& a, hipStream_t s) {
   if (hipGetDevice(&dev) != hipSuccess) dev = 32;
 #define TP_LAUNCH(E)                                                                         \
   do {                                                                                       \
-    auto* fn = gemm_dma_kernel<BM, BN, BK, WGM, WGN, A_KC, B_KC, E, SPLIT, STAGES, SB>;    \
+    auto* fn = gemm_dma_kernel<BM, BN, BK, WGM, WGN, A_KC, B_KC, E, SPLIT, STAGES, SB, F16>;\
     static std::atomic<uint32_t> attr_set{0};                                                \
     const uint32_t bit = dev < 32 ? 1u << dev : 0u;                                          \
     if (!bit || !(attr_set.load(std::memory_order_acquire) & bit)) {                         \
@@ -589,6 +529,10 @@ hipError_t launch_dma(const GemmArgs& a, hipStream_t s) {
   } while (0)
   if constexpr (SPLIT) {
     TP_LAUNCH(EPI_STORE);
+  } else if constexpr (F16) {
+    // fp16 operands: only the query/key/value product
+    if (a.epi != EPI_QKV) return hipErrorNotSupported;
+    TP_LAUNCH(EPI_QKV);
   } else if constexpr (!A_KC && !B_KC) {
     // m/n-contiguous operands on both sides: the weight-gradient products
     switch (a.epi) {
@@ -619,7 +563,7 @@ hipError_t launch_dma(const GemmArgs& a, hipStream_t s) {
 // otherwise the split count comes from the cost model below (<= 8 splits of
 // >= 8 k-tiles).
 template <int BM, int BN, int BK, int WGM, int WGN, bool A_KC, bool B_KC, int STAGES,
-          int SB = STAGES>
+          int SB, bool F16>
 hipError_t run_dma(GemmArgs a, hipStream_t s, int force_splits = 0) {
   constexpr int CUS = 256;
   if (a.K % BK) return hipErrorNotSupported;
@@ -647,25 +591,25 @@ hipError_t run_dma(GemmArgs a, hipStream_t s, int force_splits = 0) {
   if (splits > 1) {
     a.k_split = cdiv(nkt, splits) * BK;
     a.splits = cdiv(a.K, a.k_split);
-    hipError_t e = launch_dma<BM, BN, BK, WGM, WGN, A_KC, B_KC, STAGES, SB, true>(a, s);
+    hipError_t e = launch_dma<BM, BN, BK, WGM, WGN, A_KC, B_KC, STAGES, SB, true, F16>(a, s);
     if (e != hipSuccess) return e;
     return gemm_splitk_reduce(a, s);
   }
   // many tiles: XCD-aware super-tile order
   if (tiles >= 2 * CUS) a.walk = 1;
-  return launch_dma<BM, BN, BK, WGM, WGN, A_KC, B_KC, STAGES, SB, false>(a, s);
+  return launch_dma<BM, BN, BK, WGM, WGN, A_KC, B_KC, STAGES, SB, false, F16>(a, s);
 }
 
-template <bool A_KC, bool B_KC>
+template <bool A_KC, bool B_KC, bool F16 = false>
 hipError_t run_cfg_id(int cfg, const GemmArgs& a, hipStream_t s, int splits = 0) {
   switch (cfg) {
-    case 0: return run_dma<128, 128, 64, 2, 2, A_KC, B_KC, 4>(a, s, splits);
-    case 1: return run_dma<256, 128, 64, 4, 2, A_KC, B_KC, 3>(a, s, splits);
-    case 2: return run_dma<256, 256, 64, 2, 4, A_KC, B_KC, 2>(a, s, splits);
-    case 3: return run_dma<256, 256, 64, 2, 4, A_KC, B_KC, 2, 3>(a, s, splits);
+    case 0: return run_dma<128, 128, 64, 2, 2, A_KC, B_KC, 4, 4, F16>(a, s, splits);
+    case 1: return run_dma<256, 128, 64, 4, 2, A_KC, B_KC, 3, 3, F16>(a, s, splits);
+    case 2: return run_dma<256, 256, 64, 2, 4, A_KC, B_KC, 2, 2, F16>(a, s, splits);
+    case 3: return run_dma<256, 256, 64, 2, 4, A_KC, B_KC, 2, 3, F16>(a, s, splits);
     case 4:
       // 256 x 192: 256 tiles for a 256-row product of width 49152, 64 for 12288
-      if constexpr (A_KC) return run_dma<256, 192, 64, 4, 2, A_KC, B_KC, 2, 3>(a, s, splits);
+      if constexpr (A_KC) return run_dma<256, 192, 64, 4, 2, A_KC, B_KC, 2, 3, F16>(a, s, splits);
       else return hipErrorNotSupported;
     default: return hipErrorNotSupported;
   }
@@ -747,6 +691,12 @@ hipError_t gemm_dma_bf16_cfg(int cfg, const GemmArgs& a, hipStream_t s) {
       cfg = c.cfg;
       splits = c.splits;
     }
+  }
+  if (a.in_f16) {
+    // fp16 operands: the query/key/value product (activations times the fp16
+    // weight copy, both k-contiguous)
+    if (!(a_kc && b_kc) || a.epi != EPI_QKV) return hipErrorNotSupported;
+    return run_cfg_id<true, true, true>(cfg, a, s, splits);
   }
   if (a_kc && b_kc) return run_cfg_id<true, true>(cfg, a, s, splits);
   if (a_kc && b_nc) return run_cfg_id<true, false>(cfg, a, s, splits);

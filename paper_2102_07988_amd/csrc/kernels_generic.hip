@@ -4,40 +4,10 @@
 // These carry the fp32 validation mode and every shape the bf16 fast kernels
 // do not take.
 #include "tp_common.hpp"
+#include "tp_epilogue.hpp"
 #include "tp_kernels.hpp"
 
 namespace tp {
-
-// ------------------------------------------------------------------ epilogue
-
-template <typename T, int EPI>
-__device__ inline void gemm_epilogue(const GemmArgs& a, int m, int n, float acc) {
-  if constexpr (EPI == EPI_ACC_F32) {
-    float* C = (float*)a.C + (long)m * a.ldc + n;
-    *C += acc;
-  } else if constexpr (EPI == EPI_DGELU) {
-    const float z = ld((const T*)a.R + (long)m * a.ldr + n);
-    st((T*)a.C + (long)m * a.ldc + n, acc * gelu_tanh_grad(z));
-  } else {
-    const float v = acc + (a.bias ? ld((const T*)a.bias + n) : 0.f);
-    if constexpr (EPI == EPI_STORE) {
-      st((T*)a.C + (long)m * a.ldc + n, v);
-    } else if constexpr (EPI == EPI_RESID) {
-      st((T*)a.C + (long)m * a.ldc + n, v + ld((const T*)a.R + (long)m * a.ldr + n));
-    } else if constexpr (EPI == EPI_GELU) {
-      st((T*)a.C + (long)m * a.ldc + n, v);
-      st((T*)a.C2 + (long)m * a.ldc2 + n, gelu_tanh(v));
-    } else if constexpr (EPI == EPI_QKV) {
-      const int H = a.H;
-      if (n < H)
-        st((T*)a.q + (long)m * H + n, v);
-      else if (n < 2 * H)
-        st((T*)a.k + (long)m * H + (n - H), v);
-      else
-        st((T*)a.v + (long)m * H + (n - 2 * H), v);
-    }
-  }
-}
 
 // ------------------------------------------------------------- generic GEMM
 
@@ -96,7 +66,7 @@ __global__ __launch_bounds__(256) void gemm_generic_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int m = m0 + ty + 16 * i, n = n0 + tx + 16 * j;
-      if (m < a.M && n < a.N) gemm_epilogue<T, EPI>(a, m, n, acc[i][j]);
+      if (m < a.M && n < a.N) epi1<T, EPI>(a, m, n, acc[i][j]);
     }
 }
 
@@ -274,13 +244,17 @@ inline LnShape ln_shape(int H) {
   return {cpt, cdiv(cdiv(nc, cpt), 64) * 64};
 }
 
-template <typename T, int CPT>
-__global__ __launch_bounds__(1024) void ln_fwd_kernel(int H, const T* x, T* x_copy, const T* g,
-                                                      const T* b, T* u, float* mean, float* rstd,
+// T: stage dtype (gamma, beta, u); TX: type of the input rows x (fp32 for the
+// residual stream of a mixed-precision stage).  x_copy (fp32 when copy_f32, else
+// T) and u16 (fp16 copy of u) are optional.
+template <typename T, typename TX, int CPT>
+__global__ __launch_bounds__(1024) void ln_fwd_kernel(int H, const TX* x, void* x_copy,
+                                                      int copy_f32, const T* g, const T* b, T* u,
+                                                      f16s* u16, float* mean, float* rstd,
                                                       float eps) {
   __shared__ float red[16];
   const int row = blockIdx.x, nc = H >> 3, nt = blockDim.x;
-  const T* xr = x + (long)row * H;
+  const TX* xr = x + (long)row * H;
   float v[CPT][8], gg[CPT][8], bb[CPT][8];
 #pragma unroll
   for (int c = 0; c < CPT; ++c) {
@@ -313,7 +287,13 @@ __global__ __launch_bounds__(1024) void ln_fwd_kernel(int H, const T* x, T* x_co
 #pragma unroll
       for (int e = 0; e < 8; ++e) o[e] = gg[c][e] * ((v[c][e] - mu) * rs) + bb[c][e];
       store8(u + (long)row * H + ci * 8, o);
-      if (x_copy) store8(x_copy + (long)row * H + ci * 8, v[c]);
+      if (u16) st8(u16 + (long)row * H + ci * 8, o);
+      if (x_copy) {
+        if (copy_f32)
+          store8((float*)x_copy + (long)row * H + ci * 8, v[c]);
+        else
+          store8((T*)x_copy + (long)row * H + ci * 8, v[c]);
+      }
     }
   }
   if (threadIdx.x == 0) {
@@ -334,8 +314,8 @@ __device__ inline float2 block_sum2(float a, float b, float* red /* >= 32 floats
   return make_float2(sa, sb);
 }
 
-template <typename T, int CPT>
-__global__ __launch_bounds__(1024) void ln_bwd_kernel(int H, const T* du, const T* x,
+template <typename T, typename TX, int CPT>
+__global__ __launch_bounds__(1024) void ln_bwd_kernel(int H, const T* du, const TX* x,
                                                       const float* mean, const float* rstd,
                                                       const T* g, const T* resid, T* dx) {
   __shared__ float red[32];
@@ -402,9 +382,9 @@ __device__ inline float col_partials_sum(float (*p)[CR_COLS + 1], float* q /* 8 
   return t;
 }
 
-template <typename T>
+template <typename T, typename TX>
 __global__ __launch_bounds__(256) void ln_param_grads_kernel(int n, int H, const T* du,
-                                                             const T* x, const float* mean,
+                                                             const TX* x, const float* mean,
                                                              const float* rstd, float* dg,
                                                              float* db) {
   __shared__ float pg[CR_RG][CR_COLS + 1], pb[CR_RG][CR_COLS + 1], q[2][8 * (CR_COLS + 1)];
@@ -504,52 +484,87 @@ __global__ void copy_kernel(size_t n, const T* src, T* dst) {
     dst[e] = src[e];
 }
 
-hipError_t ln_fwd(int dtype, int n, int H, const void* x, void* x_copy, const void* g,
-                  const void* b, void* u, float* mean, float* rstd, float eps, hipStream_t s) {
+hipError_t ln_fwd(int dtype, int n, int H, const void* x, int x_f32, void* x_copy, int copy_f32,
+                  const void* g, const void* b, void* u, void* u16, float* mean, float* rstd,
+                  float eps, hipStream_t s) {
   clear_stale_error();
   if (n <= 0) return hipSuccess;
   const LnShape sh = ln_shape(H);
-#define TP_LN(TT, C)                                                                        \
-  ln_fwd_kernel<TT, C><<<n, sh.nt, 0, s>>>(H, (const TT*)x, (TT*)x_copy, (const TT*)g,      \
-                                           (const TT*)b, (TT*)u, mean, rstd, eps)
+#define TP_LN(TT, TX, C)                                                                   \
+  ln_fwd_kernel<TT, TX, C><<<n, sh.nt, 0, s>>>(H, (const TX*)x, x_copy, copy_f32,           \
+                                               (const TT*)g, (const TT*)b, (TT*)u,          \
+                                               (f16s*)u16, mean, rstd, eps)
   if (dtype == DT_FP32) {
-    if (sh.cpt == 1) TP_LN(float, 1); else TP_LN(float, 2);
+    if (sh.cpt == 1) TP_LN(float, float, 1); else TP_LN(float, float, 2);
+  } else if (x_f32) {
+    if (sh.cpt == 1) TP_LN(bf16, float, 1); else TP_LN(bf16, float, 2);
   } else {
-    if (sh.cpt == 1) TP_LN(bf16, 1); else TP_LN(bf16, 2);
+    if (sh.cpt == 1) TP_LN(bf16, bf16, 1); else TP_LN(bf16, bf16, 2);
   }
 #undef TP_LN
   return hipGetLastError();
 }
 
-hipError_t ln_bwd(int dtype, int n, int H, const void* du, const void* x, const float* mean,
-                  const float* rstd, const void* g, const void* resid, void* dx, hipStream_t s) {
+hipError_t ln_bwd(int dtype, int n, int H, const void* du, const void* x, int x_f32,
+                  const float* mean, const float* rstd, const void* g, const void* resid, void* dx,
+                  hipStream_t s) {
   clear_stale_error();
   if (n <= 0) return hipSuccess;
   const LnShape sh = ln_shape(H);
-#define TP_LN(TT, C)                                                                        \
-  ln_bwd_kernel<TT, C><<<n, sh.nt, 0, s>>>(H, (const TT*)du, (const TT*)x, mean, rstd,      \
-                                           (const TT*)g, (const TT*)resid, (TT*)dx)
+#define TP_LN(TT, TX, C)                                                                   \
+  ln_bwd_kernel<TT, TX, C><<<n, sh.nt, 0, s>>>(H, (const TT*)du, (const TX*)x, mean, rstd,  \
+                                               (const TT*)g, (const TT*)resid, (TT*)dx)
   if (dtype == DT_FP32) {
-    if (sh.cpt == 1) TP_LN(float, 1); else TP_LN(float, 2);
+    if (sh.cpt == 1) TP_LN(float, float, 1); else TP_LN(float, float, 2);
+  } else if (x_f32) {
+    if (sh.cpt == 1) TP_LN(bf16, float, 1); else TP_LN(bf16, float, 2);
   } else {
-    if (sh.cpt == 1) TP_LN(bf16, 1); else TP_LN(bf16, 2);
+    if (sh.cpt == 1) TP_LN(bf16, bf16, 1); else TP_LN(bf16, bf16, 2);
   }
 #undef TP_LN
   return hipGetLastError();
 }
 
-hipError_t ln_param_grads(int dtype, int n, int H, const void* du, const void* x,
+hipError_t ln_param_grads(int dtype, int n, int H, const void* du, const void* x, int x_f32,
                           const float* mean, const float* rstd, float* dg, float* db,
                           hipStream_t s) {
   clear_stale_error();
   if (n <= 0) return hipSuccess;
   const int blocks = cdiv(H, CR_COLS);
   if (dtype == DT_FP32)
-    ln_param_grads_kernel<float><<<blocks, 256, 0, s>>>(n, H, (const float*)du, (const float*)x,
-                                                        mean, rstd, dg, db);
+    ln_param_grads_kernel<float, float><<<blocks, 256, 0, s>>>(n, H, (const float*)du,
+                                                               (const float*)x, mean, rstd, dg, db);
+  else if (x_f32)
+    ln_param_grads_kernel<bf16, float><<<blocks, 256, 0, s>>>(n, H, (const bf16*)du,
+                                                              (const float*)x, mean, rstd, dg, db);
   else
-    ln_param_grads_kernel<bf16><<<blocks, 256, 0, s>>>(n, H, (const bf16*)du, (const bf16*)x,
-                                                       mean, rstd, dg, db);
+    ln_param_grads_kernel<bf16, bf16><<<blocks, 256, 0, s>>>(n, H, (const bf16*)du,
+                                                             (const bf16*)x, mean, rstd, dg, db);
+  return hipGetLastError();
+}
+
+// 8 bf16 values per thread as fp16 (n % 8 == 0, 16-byte aligned), else one.
+__global__ void cvt_bf16_f16_kernel(size_t n, const uint16_t* src, uint16_t* dst, int vec) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  if (vec) {
+    for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < n / 8; e += stride) {
+      float v[8];
+      ld8((const bf16*)src + 8 * e, v);
+      st8((f16s*)dst + 8 * e, v);
+    }
+  } else {
+    for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += stride)
+      dst[e] = f32_to_f16_bits(to_f32(bf16{src[e]}));
+  }
+}
+
+hipError_t cvt_bf16_f16(size_t n, const void* src, void* dst, hipStream_t s) {
+  clear_stale_error();
+  if (n == 0) return hipSuccess;
+  const int vec = n % 8 == 0 && ((uintptr_t)src & 15) == 0 && ((uintptr_t)dst & 15) == 0;
+  const size_t work = vec ? n / 8 : n;
+  const int blocks = (int)((work + 255) / 256 < 8192 ? (work + 255) / 256 : 8192);
+  cvt_bf16_f16_kernel<<<blocks, 256, 0, s>>>(n, (const uint16_t*)src, (uint16_t*)dst, vec);
   return hipGetLastError();
 }
 

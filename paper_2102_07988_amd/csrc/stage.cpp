@@ -29,6 +29,9 @@ struct LayerBufs {
   // per-token LayerNorm output gradients (DEFERRED mode: inputs of the
   // LayerNorm-parameter gradients, reduced once per sequence)
   void *du2, *du;
+  // mixed-precision path only: fp16 copy of the LN1 output, bf16 copy of the
+  // values (the backward's), fp16 copy of W_qkv (taken at the sequence start)
+  void *u16, *vb, *w16;
 };
 
 struct Scratch {
@@ -72,6 +75,8 @@ struct tp_stage {
   int H, A, F, heads, d, L, dt;
   int bsz;  // sequences per batch slice: token t of sequence s is row t * bsz + s
   size_t esz;
+  bool mixed;   // mixed-precision path (see mixed_of)
+  size_t resz;  // element size of the residual stream (fp32 on the mixed path)
   std::vector<tp_layer_ptrs> P, G;
   std::vector<LayerBufs> lb;
   Scratch sc;
@@ -104,6 +109,13 @@ bool config_ok(const tp_stage_config* c) {
 
 int batch_of(const tp_stage_config* c) { return c->batch > 0 ? c->batch : 1; }
 int parts_of(const tp_stage_config* c) { return c->op_parts > 0 ? c->op_parts : 1; }
+// The mixed-precision path of bf16 stages whose head width the matrix-core
+// attention takes (64, 128): residual stream in fp32, fp16 operands for the
+// query/key/value product and the attention scores.
+bool mixed_of(const tp_stage_config* c) {
+  const int d = c->hidden / c->heads;
+  return c->dtype == TP_DTYPE_BF16 && (d == 64 || d == 128);
+}
 
 bool config_supported(const tp_stage_config* c) {
   const int d = c->hidden / c->heads;
@@ -117,18 +129,20 @@ bool config_supported(const tp_stage_config* c) {
 size_t carve(const tp_stage_config* c, void* base, std::vector<LayerBufs>* lbs, Scratch* sc) {
   Carver cv(base);
   const size_t esz = c->dtype == TP_DTYPE_FP32 ? 4 : 2;
+  const bool mixed = mixed_of(c);
+  const size_t resz = mixed ? 4 : esz;  // residual stream (layer inputs, x1)
   // every per-token arena holds max_seq * batch rows
   const size_t L = (size_t)c->max_seq * batch_of(c), H = c->hidden, pp = parts_of(c);
   const size_t a = c->heads / pp, A = a * (H / c->heads), F = 4 * H / pp;
   for (int i = 0; i < c->n_layers; ++i) {
     LayerBufs b;
-    b.x_in = cv.take(L * H * esz);
+    b.x_in = cv.take(L * H * resz);
     b.u = cv.take(L * H * esz);
     b.q = cv.take(L * A * esz);
     b.kc = cv.take(L * A * esz);
     b.vc = cv.take(L * A * esz);
     b.o = cv.take(L * A * esz);
-    b.x1 = cv.take(L * H * esz);
+    b.x1 = cv.take(L * H * resz);
     b.u2 = cv.take(L * H * esz);
     b.z = cv.take(L * F * esz);
     b.g = cv.take(L * F * esz);
@@ -148,6 +162,13 @@ size_t carve(const tp_stage_config* c, void* base, std::vector<LayerBufs>* lbs, 
       b.du = cv.take(L * H * esz);
     } else {
       b.du2 = b.du = nullptr;
+    }
+    if (mixed) {
+      b.u16 = cv.take(L * H * 2);
+      b.vb = cv.take(L * A * 2);
+      b.w16 = cv.take(3 * A * H * 2);
+    } else {
+      b.u16 = b.vb = b.w16 = nullptr;
     }
     if (lbs) lbs->push_back(b);
   }
@@ -293,17 +314,31 @@ tp_status deferred_param_reductions(tp_stage* S, int li, int rows) {
   TRY(launch(S, K_MISC, 0, (double)rows * F * e,
              [&] { return colsum_acc(dt, rows, F, B.dz, F, (float*)G.b_fc1, st); }));
   TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
-    return ln_param_grads(dt, rows, H, B.du2, B.x1, B.mean2, B.rstd2, (float*)G.ln2_g,
+    return ln_param_grads(dt, rows, H, B.du2, B.x1, S->mixed, B.mean2, B.rstd2, (float*)G.ln2_g,
                           (float*)G.ln2_b, st);
   }));
   TRY(launch(S, K_MISC, 0, nb, [&] { return colsum_acc(dt, rows, H, B.dx1, H, (float*)G.b_o, st); }));
   TRY(launch(S, K_MISC, 0, 3.0 * rows * A * e,
              [&] { return colsum_acc(dt, rows, 3 * A, B.dqkv, 3 * A, (float*)G.b_qkv, st); }));
   TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
-    return ln_param_grads(dt, rows, H, B.du, B.x_in, B.mean1, B.rstd1, (float*)G.ln1_g,
+    return ln_param_grads(dt, rows, H, B.du, B.x_in, S->mixed, B.mean1, B.rstd1, (float*)G.ln1_g,
                           (float*)G.ln1_b, st);
   }));
   return TP_OK;
+}
+
+// Mixed-precision path: fp16 copies of every layer's W_qkv for the
+// query/key/value product, taken at the start of a sequence (the parameters
+// stay fixed while its slices run).
+hipError_t snapshot_wqkv(tp_stage* S) {
+  if (!S->mixed) return hipSuccess;
+  const size_t n = (size_t)3 * S->A * S->H;
+  for (int li = 0; li < S->cfg.n_layers; ++li) {
+    const hipError_t e = launch(S, K_MISC, 0, 4.0 * n,
+                                [&] { return cvt_bf16_f16(n, S->P[li].w_qkv, S->lb[li].w16, S->stream); });
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 tp_status forward_impl(tp_stage* S, int l, int r, const void* x, void* y) {
@@ -316,15 +351,21 @@ tp_status forward_impl(tp_stage* S, int l, int r, const void* x, void* y) {
   for (int li = 0; li < NL; ++li) {
     LayerBufs& B = S->lb[li];
     const tp_layer_ptrs& P = S->P[li];
-    void* xin = rowp(B.x_in, lr, H, e);
+    const bool mx = S->mixed;
+    const size_t re = S->resz;
+    void* xin = rowp(B.x_in, lr, H, re);
+    void* x1 = rowp(B.x1, lr, H, re);
     TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
-      return ln_fwd(dt, n, H, li == 0 ? x : xin, li == 0 ? xin : nullptr, P.ln1_g, P.ln1_b,
-                    rowp(B.u, lr, H, e), B.mean1 + lr, B.rstd1 + lr, S->cfg.ln_eps, st);
+      return ln_fwd(dt, n, H, li == 0 ? x : xin, li > 0 && mx, li == 0 ? xin : nullptr, mx,
+                    P.ln1_g, P.ln1_b, rowp(B.u, lr, H, e), mx ? rowp(B.u16, lr, H, 2) : nullptr,
+                    B.mean1 + lr, B.rstd1 + lr, S->cfg.ln_eps, st);
     }));
-    GemmArgs g = nt(n, 3 * A, H, rowp(B.u, lr, H, e), H, P.w_qkv);
+    GemmArgs g = mx ? nt(n, 3 * A, H, rowp(B.u16, lr, H, 2), H, B.w16)
+                    : nt(n, 3 * A, H, rowp(B.u, lr, H, e), H, P.w_qkv);
     g.epi = EPI_QKV;
     g.bias = P.b_qkv;
     g.q = rowp(B.q, lr, A, e), g.k = rowp(B.kc, lr, A, e), g.v = rowp(B.vc, lr, A, e), g.H = A;
+    if (mx) g.in_f16 = 1, g.qkv_f16 = 1, g.vb = rowp(B.vb, lr, A, 2);
     TRY(run_gemm(S, K_GEMM_FWD, g));
     AttnArgs a;
     a.l = l, a.r = r, a.H = A, a.heads = S->heads, a.d = S->d, a.Lmax = S->L;
@@ -332,23 +373,26 @@ tp_status forward_impl(tp_stage* S, int l, int r, const void* x, void* y) {
     a.ws = S->sc.attn, a.ws_elems = (long)S->sc.attn_elems;
     a.scale = 1.f / std::sqrt((float)S->d);
     a.q = rowp(B.q, lr, A, e), a.kc = B.kc, a.vc = B.vc, a.o = rowp(B.o, lr, A, e), a.lse = B.lse;
+    a.f16 = mx;
     const double pairs = ((double)ntok * l + (double)ntok * (ntok + 1) / 2) * S->bsz;
     TRY(launch(S, K_ATTN_FWD, 4.0 * A * pairs, (2.0 * ntok + 2.0 * r) * S->bsz * A * e,
                [&] { return attn_fwd(dt, a, st); }));
     g = nt(n, H, A, rowp(B.o, lr, A, e), A, P.w_o);
-    g.epi = EPI_RESID, g.bias = P.b_o, g.R = xin, g.ldr = H, g.C = rowp(B.x1, lr, H, e), g.ldc = H;
+    g.epi = EPI_RESID, g.bias = P.b_o, g.R = xin, g.ldr = H, g.C = x1, g.ldc = H;
+    g.r_f32 = g.c_f32 = mx;
     TRY(run_gemm(S, K_GEMM_FWD, g));
     TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
-      return ln_fwd(dt, n, H, rowp(B.x1, lr, H, e), nullptr, P.ln2_g, P.ln2_b,
-                    rowp(B.u2, lr, H, e), B.mean2 + lr, B.rstd2 + lr, S->cfg.ln_eps, st);
+      return ln_fwd(dt, n, H, x1, mx, nullptr, 0, P.ln2_g, P.ln2_b, rowp(B.u2, lr, H, e), nullptr,
+                    B.mean2 + lr, B.rstd2 + lr, S->cfg.ln_eps, st);
     }));
     g = nt(n, F, H, rowp(B.u2, lr, H, e), H, P.w_fc1);
     g.epi = EPI_GELU, g.bias = P.b_fc1, g.C = rowp(B.z, lr, F, e), g.ldc = F;
     g.C2 = rowp(B.g, lr, F, e), g.ldc2 = F;
     TRY(run_gemm(S, K_GEMM_FWD, g));
     g = nt(n, H, F, rowp(B.g, lr, F, e), F, P.w_fc2);
-    g.epi = EPI_RESID, g.bias = P.b_fc2, g.R = rowp(B.x1, lr, H, e), g.ldr = H;
-    g.C = li == NL - 1 ? y : rowp(S->lb[li + 1].x_in, lr, H, e), g.ldc = H;
+    g.epi = EPI_RESID, g.bias = P.b_fc2, g.R = x1, g.ldr = H, g.r_f32 = mx;
+    g.C = li == NL - 1 ? y : rowp(S->lb[li + 1].x_in, lr, H, re), g.ldc = H;
+    g.c_f32 = mx && li < NL - 1;
     TRY(run_gemm(S, K_GEMM_FWD, g));
   }
   return TP_OK;
@@ -362,11 +406,14 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
   hipStream_t st = S->stream;
   const bool per_slice = S->cfg.wgrad_mode == TP_WGRAD_PER_SLICE;
   const double nb = (double)n * H * e;
+  const bool mx = S->mixed;
   for (int li = NL - 1; li >= 0; --li) {
     LayerBufs& B = S->lb[li];
     const tp_layer_ptrs& P = S->P[li];
     tp_layer_ptrs& G = S->G[li];
     void* dyl = rowp(B.dy, lr, H, e);
+    const void* x1 = rowp(B.x1, lr, H, S->resz);
+    const void* xin = rowp(B.x_in, lr, H, S->resz);
     if (li == NL - 1)
       TRY(launch(S, K_MISC, 0, 2 * nb, [&] { return copy_rows(dt, n, H, dy, dyl, st); }));
     // FC2 backward (dX fused with GELU'): dz = (dy W2) * GELU'(z)
@@ -389,12 +436,12 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
       }));
     // LN2 backward + residual: dx1 = dy + LN2^T(du2)
     TRY(launch(S, K_NORM, 0, 4 * nb, [&] {
-      return ln_bwd(dt, n, H, du2, rowp(B.x1, lr, H, e), B.mean2 + lr, B.rstd2 + lr, P.ln2_g,
+      return ln_bwd(dt, n, H, du2, x1, mx, B.mean2 + lr, B.rstd2 + lr, P.ln2_g,
                     dyl, rowp(B.dx1, lr, H, e), st);
     }));
     if (per_slice)
       TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
-        return ln_param_grads(dt, n, H, du2, rowp(B.x1, lr, H, e), B.mean2 + lr, B.rstd2 + lr,
+        return ln_param_grads(dt, n, H, du2, x1, mx, B.mean2 + lr, B.rstd2 + lr,
                               (float*)G.ln2_g, (float*)G.ln2_b, st);
       }));
     // output projection backward: dO = dx1 W_o
@@ -411,7 +458,9 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
     a.bs = S->bsz, a.ld = S->bsz * A;
     a.ws = S->sc.attn, a.ws_elems = (long)S->sc.attn_elems;
     a.scale = 1.f / std::sqrt((float)S->d);
-    a.q = rowp(B.q, lr, A, e), a.kc = B.kc, a.vc = B.vc, a.o = rowp(B.o, lr, A, e), a.lse = B.lse;
+    a.q = rowp(B.q, lr, A, e), a.kc = B.kc, a.o = rowp(B.o, lr, A, e), a.lse = B.lse;
+    a.vc = mx ? B.vb : B.vc;  // the backward's values are bf16
+    a.f16 = mx;
     a.dout = S->sc.dout, a.D = S->sc.D;
     a.dq = rowp(B.dqkv, lr, 3 * A, e), a.ld_dq = (long)S->bsz * 3 * A, a.dq_seq = 3 * A;
     a.dk = B.dk, a.dv = B.dv;
@@ -434,12 +483,12 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
     // LN1 backward + residual: dx = dx1 + LN1^T(du)
     void* out = li == 0 ? dx : rowp(S->lb[li - 1].dy, lr, H, e);
     TRY(launch(S, K_NORM, 0, 4 * nb, [&] {
-      return ln_bwd(dt, n, H, du, rowp(B.x_in, lr, H, e), B.mean1 + lr, B.rstd1 + lr, P.ln1_g,
+      return ln_bwd(dt, n, H, du, xin, mx, B.mean1 + lr, B.rstd1 + lr, P.ln1_g,
                     rowp(B.dx1, lr, H, e), out, st);
     }));
     if (per_slice)
       TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
-        return ln_param_grads(dt, n, H, du, rowp(B.x_in, lr, H, e), B.mean1 + lr, B.rstd1 + lr,
+        return ln_param_grads(dt, n, H, du, xin, mx, B.mean1 + lr, B.rstd1 + lr,
                               (float*)G.ln1_g, (float*)G.ln1_b, st);
       }));
     if (per_slice) {
@@ -498,6 +547,8 @@ tp_status tp_stage_init(const tp_stage_config* cfg, const tp_layer_ptrs* params,
   S->bsz = batch_of(cfg);
   S->dt = cfg->dtype == TP_DTYPE_FP32 ? DT_FP32 : DT_BF16;
   S->esz = cfg->dtype == TP_DTYPE_FP32 ? 4 : 2;
+  S->mixed = mixed_of(cfg);
+  S->resz = S->mixed ? 4 : S->esz;
   S->P.assign(params, params + cfg->n_layers);
   S->G.assign(grads, grads + cfg->n_layers);
   carve(cfg, workspace, &S->lb, &S->sc);
@@ -523,6 +574,7 @@ tp_status tp_kv_prefix_reset(tp_stage* S) {
     TRY(fill_f32(B.dk, n, 0.f, S->stream));
     TRY(fill_f32(B.dv, n, 0.f, S->stream));
   }
+  TRY(snapshot_wqkv(S));
   S->cached_len = 0;
   S->bwd_frontier = 0;
   return TP_OK;
@@ -573,7 +625,7 @@ tp_status tp_profile_slice_cost(tp_stage* S, const int* lens, int n_lens, const 
   const bool was_timing = S->timing;
   S->timing = false;
   S->profiling = true;
-  tp_status status = TP_OK;
+  tp_status status = snapshot_wqkv(S) == hipSuccess ? TP_OK : TP_ERR_HIP;
   // deterministic, finite slice inputs
   const size_t io = (size_t)S->L * S->bsz * S->H;
   if (S->dt == DT_FP32) {

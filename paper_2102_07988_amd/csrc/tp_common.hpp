@@ -38,6 +38,20 @@ __host__ __device__ inline uint16_t f32_to_bf16_bits(float f) {
   return (uint16_t)(u >> 16);
 }
 
+// fp16 carried as raw 16-bit storage too (the stage's mixed-precision path
+// keeps the operands of the query/key/value product and of the attention
+// scores in fp16); conversions round to nearest even.
+struct f16s {
+  uint16_t v;
+};
+__host__ __device__ inline uint16_t f32_to_f16_bits(float f) {
+  return __builtin_bit_cast(uint16_t, (_Float16)f);
+}
+__host__ __device__ inline float f16_bits_to_f32(uint16_t b) {
+  return (float)__builtin_bit_cast(_Float16, b);
+}
+__host__ __device__ inline float to_f32(f16s x) { return f16_bits_to_f32(x.v); }
+
 template <typename T>
 __host__ __device__ inline T from_f32(float x);
 template <>
@@ -49,6 +63,13 @@ __host__ __device__ inline bf16 from_f32<bf16>(float x) {
   bf16 b;
   b.v = f32_to_bf16_bits(x);
   return b;
+}
+
+template <>
+__host__ __device__ inline f16s from_f32<f16s>(float x) {
+  f16s h;
+  h.v = f32_to_f16_bits(x);
+  return h;
 }
 
 template <typename T>
@@ -119,6 +140,21 @@ __device__ inline void st8(bf16* p, const float* x) {
   for (int i = 0; i < 4; ++i)
     w[i] = (uint32_t)f32_to_bf16_bits(x[2 * i]) | ((uint32_t)f32_to_bf16_bits(x[2 * i + 1]) << 16);
   *(uint4*)p = make_uint4(w[0], w[1], w[2], w[3]);
+}
+__device__ inline void st8(f16s* p, const float* x) {
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    w[i] = (uint32_t)f32_to_f16_bits(x[2 * i]) | ((uint32_t)f32_to_f16_bits(x[2 * i + 1]) << 16);
+  *(uint4*)p = make_uint4(w[0], w[1], w[2], w[3]);
+}
+__device__ inline void ld8(const float* p, float* x) {
+  const float4 a = ((const float4*)p)[0], b = ((const float4*)p)[1];
+  x[0] = a.x, x[1] = a.y, x[2] = a.z, x[3] = a.w, x[4] = b.x, x[5] = b.y, x[6] = b.z, x[7] = b.w;
+}
+__device__ inline void st8(float* p, const float* x) {
+  ((float4*)p)[0] = make_float4(x[0], x[1], x[2], x[3]);
+  ((float4*)p)[1] = make_float4(x[4], x[5], x[6], x[7]);
 }
 
 __host__ __device__ inline int cdiv(long a, long b) { return (int)((a + b - 1) / b); }

@@ -37,6 +37,15 @@ struct GemmArgs {
   long ldc2 = 0;
   void *q = nullptr, *k = nullptr, *v = nullptr;  // EPI_QKV destinations, row stride H
   int H = 0;
+  // Mixed-precision path of a bf16 stage: A and B are fp16 (the query/key/value
+  // product of fp16 LayerNorm output and an fp16 copy of W_qkv); EPI_QKV then
+  // writes q, k, v as fp16 and v once more as bf16 to vb.  EPI_RESID: r_f32 /
+  // c_f32 mark an fp32 residual input / output (the residual stream of a
+  // mixed-precision stage).
+  int in_f16 = 0;
+  int qkv_f16 = 0;
+  void* vb = nullptr;
+  int r_f32 = 0, c_f32 = 0;
   // fp32 scratch for split-K partial sums (may be null: no split)
   float* ws = nullptr;
   long ws_elems = 0;
@@ -87,6 +96,11 @@ struct AttnArgs {
   int nsplit = 1, kv_chunk = 0;
   float* ws = nullptr;
   long ws_elems = 0;
+  // Mixed-precision path: q and kc hold fp16, and so does vc in the forward;
+  // scores (Q K^T) and, in the forward, P V run on fp16 operands, the dS
+  // products of the backward on fp16 dS.  The backward's vc is bf16 (dP = dO
+  // V^T and dV = P^T dO keep the gradient side in bf16).
+  int f16 = 0;
 };
 // The arguments of sequence blockIdx.z of the batch as a one-sequence view:
 // pointers moved to its columns (element type T) and planes; the row stride
@@ -111,17 +125,23 @@ __device__ inline AttnArgs attn_seq_view(AttnArgs a) {
 hipError_t attn_fwd(int dtype, const AttnArgs& a, hipStream_t s);
 hipError_t attn_bwd(int dtype, const AttnArgs& a, hipStream_t s);
 
-// LayerNorm over rows of H: u = g * (x - mean) * rstd + b.  If x_copy is not
-// null, the input rows are also copied there.
-hipError_t ln_fwd(int dtype, int n, int H, const void* x, void* x_copy, const void* g,
-                  const void* b, void* u, float* mean, float* rstd, float eps, hipStream_t s);
-// dx = LN^T(du) + resid (resid may be null).
-hipError_t ln_bwd(int dtype, int n, int H, const void* du, const void* x, const float* mean,
-                  const float* rstd, const void* g, const void* resid, void* dx, hipStream_t s);
+// LayerNorm over rows of H: u = g * (x - mean) * rstd + b.  x is fp32 when
+// x_f32, else of the stage dtype.  If x_copy is not null, the input rows are
+// also copied there (fp32 when copy_f32).  If u16 is not null, u is written
+// once more there as fp16 (bf16 stages only).
+hipError_t ln_fwd(int dtype, int n, int H, const void* x, int x_f32, void* x_copy, int copy_f32,
+                  const void* g, const void* b, void* u, void* u16, float* mean, float* rstd,
+                  float eps, hipStream_t s);
+// dx = LN^T(du) + resid (resid may be null); x fp32 when x_f32.
+hipError_t ln_bwd(int dtype, int n, int H, const void* du, const void* x, int x_f32,
+                  const float* mean, const float* rstd, const void* g, const void* resid, void* dx,
+                  hipStream_t s);
 // dg[i] += sum_t du[t][i] * xhat[t][i];  db[i] += sum_t du[t][i]   (fp32 outputs)
-hipError_t ln_param_grads(int dtype, int n, int H, const void* du, const void* x,
+hipError_t ln_param_grads(int dtype, int n, int H, const void* du, const void* x, int x_f32,
                           const float* mean, const float* rstd, float* dg, float* db,
                           hipStream_t s);
+// dst[i] = fp16(src[i]) for n bf16 values (round to nearest even).
+hipError_t cvt_bf16_f16(size_t n, const void* src, void* dst, hipStream_t s);
 // out[j] += sum_{i<n} A[i*lda + j], j < N (fp32 output)
 hipError_t colsum_acc(int dtype, int n, int N, const void* A, long lda, float* out, hipStream_t s);
 // dqkv[i][H + j] = dk[l+i][j], dqkv[i][2H + j] = dv[l+i][j] (stage dtype <- fp32)

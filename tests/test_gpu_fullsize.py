@@ -4,18 +4,18 @@ slicing), on the same seeded inputs it draws on the device.
 
 * GPT-3-1.3B stage (hidden 2048, 16 heads, L = 2048, 8 x 256): every output
   against the fp64 oracle, element by element (rel-L2 <= 2e-2 per tensor).
-* GPT-3-13B stage (hidden 5120, 40 heads, L = 2048, 8 x 256) and GPT-3-175B
-  stage (hidden 12288, 96 heads) at L = 2048 (8 x 256) and L = 8192
-  (16 x 512): the oracle is too slow for the whole sequence, so
-  (a) stage outputs y of tokens 0..15, which by the causal mask depend on
-  x[0..15] only, against the oracle run on those 16 tokens; (c) sampled later
-  rows (slice edges, long prefixes, seeded random tokens) against the
-  row-sampling oracle (fp64 library matrix products over tokens 0..max row,
-  pinned to the slice oracle in test_oracle_rows.py); (b) properties that
-  hold at any size: the last layer's FC2 bias gradient equals the column sums
-  of dy; per-slice and deferred weight gradients agree to fp32 summation order
-  with y and dx bit-identical; a different backward slicing gives the same
-  gradients to bf16 rounding.
+* GPT-3-175B stage at L = 8192 on the DP's slicing (the 13B and 175B stages
+  at L = 2048 are compared whole in test_gpu_fullwidth.py): the whole-sequence
+  oracle is too slow at 8192 tokens, so (a) stage outputs y of tokens 0..15,
+  which by the causal mask depend on x[0..15] only, against the oracle run on
+  those 16 tokens; (c) sampled later rows up to the last token (slice edges,
+  long prefixes, seeded random tokens) against the row-sampling oracle (fp64
+  library matrix products over tokens 0..max row, pinned to the slice oracle
+  in test_oracle_rows.py); (b) properties that hold at any size: the last
+  layer's FC2 bias gradient equals the column sums of dy; per-slice and
+  deferred weight gradients agree to fp32 summation order with y and dx
+  bit-identical; a different backward slicing gives the same gradients to
+  bf16 rounding.
 """
 import gc
 
@@ -63,15 +63,24 @@ def test_1p3b_stage_full_sequence_vs_oracle():
     compare(got, ref, TOL_BF16, "1.3B full sequence")
 
 
-@pytest.mark.parametrize("H,heads,L,slice_len", [(5120, 40, 2048, 256), (12288, 96, 2048, 256),
-                                                (12288, 96, 8192, 512)])
-def test_large_stage_bench_configuration(H, heads, L, slice_len):
+@pytest.mark.timeout(900)
+def test_175b_long_context_dp_slicing():
+    """GPT-3-175B stage at 8192 tokens on the DP's slicing (Algorithm 1 on a
+    model-mode table measured here, K = 48, 256-token grid)."""
     from oracle import OracleStage
-    n_layers = 2
-    fwd = [slice_len] * (L // slice_len)
-    print(f"case large stage: H={H} heads={heads} L={L} {len(fwd)}x{slice_len} deferred",
-          flush=True)
+    from paper_2102_07988_amd import terapipe as tp
+    n_layers, H, heads, L, unit = 2, 12288, 96, 8192, 256
     params, x, dy = _bench_inputs(n_layers, H, L)
+    st = tp.Stage(params, H, heads, L, dtype="bf16", wgrad="deferred")
+    U = L // unit
+    ks = sorted({k for k in (1, 2, U // 8, U // 4, U // 2, 3 * U // 4) if 1 <= k < U})
+    js = sorted({j for j in (1, U // 8, U // 4, U // 2, 3 * U // 4) if 1 <= j < U})
+    cost, _ = st.profile_model(L, unit, [unit * k for k in ks], [unit * j for j in js],
+                               warmup=1, reps=3)
+    fwd, _ = tp.dp_optimal_slicing(cost, unit, 48)
+    del st
+    print(f"case 175B 8k: H={H} heads={heads} L={L} DP slicing {fwd} deferred", flush=True)
+    assert sum(fwd) == L
     y, dx, g_def = _run(params, x, dy, H, heads, L, fwd)
     assert torch.isfinite(y.float()).all() and torch.isfinite(dx.float()).all()
 
@@ -92,18 +101,17 @@ def test_large_stage_bench_configuration(H, heads, L, slice_len):
     del y2, dx2, g_ps
     gc.collect()
 
-    # (b3) backward slices of twice the length
-    bwd = [2 * slice_len] * (L // (2 * slice_len))
-    _, dx3, g3 = _run(params, x, dy, H, heads, L, fwd, bwd)
+    # (b3) a different backward slicing (uniform 16 x 512)
+    _, dx3, g3 = _run(params, x, dy, H, heads, L, fwd, [512] * 16)
     e_dx = rel_l2(dx3.float().cpu().numpy(), dx.float().cpu().numpy())
     worst = max(rel_l2(g3[li][k].cpu().numpy(), g_def[li][k].cpu().numpy())
                 for li in range(n_layers) for k in PARAM_KEYS)
-    print(f"  bwd slicing {bwd[0]}: dx {e_dx:.2e}, grads worst {worst:.2e}", flush=True)
+    print(f"  bwd slicing 16 x 512: dx {e_dx:.2e}, grads worst {worst:.2e}", flush=True)
     assert e_dx < 1e-2 and worst < 1e-2
     del dx3, g3, g_def
     gc.collect()
 
-    # (a) the first 16 output rows against the oracle on x[0:16]
+    # (a) the first 16 output rows against the slice oracle on x[0:16]
     n = 16
     p64 = synth.params_f64([{k: v.cpu() for k, v in p.items()} for p in params])
     ost = OracleStage(p64, H, heads, n)
@@ -113,44 +121,18 @@ def test_large_stage_bench_configuration(H, heads, L, slice_len):
     print(f"  y[0:16] vs oracle: {err:.2e}", flush=True)
     assert err < TOL_BF16
 
-    # (c) late rows (last and first token of slices, long prefixes, a few seeded
-    # random ones) against the row-sampling oracle, which evaluates the causal
-    # stage for tokens 0..max(rows) in fp64; the 8192-token case stops at 6144
-    # tokens to bound the host's fp64 work
-    T = min(L, 6144)
-    rows = sorted({slice_len - 1, slice_len, T // 2 - 1, T // 2, T - slice_len, T - 1}
-                  | set(np.random.default_rng(L + H).integers(16, T, size=3).tolist()))
-    y_rows = stage_output_rows(p64, synth.to_f64(x[:T].cpu()), heads, rows)
+    # (c) late rows up to the last token (slice edges of the DP slicing, the
+    # last slice's first and last tokens, seeded random ones) against the
+    # row-sampling oracle, which evaluates the causal stage for tokens
+    # 0..max(rows) in fp64
+    edges = [int(v) for v in np.cumsum(fwd)[:-1]]
+    rows = sorted({edges[0] - 1, edges[0], edges[len(edges) // 2] - 1, edges[len(edges) // 2],
+                   edges[-1] - 1, edges[-1], L // 2, L - 2, L - 1}
+                  | set(np.random.default_rng(L + H).integers(16, L, size=3).tolist()))
+    print(f"  row oracle over {L} tokens, rows {rows}", flush=True)
+    y_rows = stage_output_rows(p64, synth.to_f64(x.cpu()), heads, rows)
     del p64
     gc.collect()
     err = rel_l2(y[rows].float().cpu().numpy(), y_rows)
     print(f"  y{rows} vs row oracle: {err:.2e}", flush=True)
     assert err < TOL_BF16
-
-
-def test_fp32_validation_mode_full_175b_rows():
-    """The fp32 validation mode at the GPT-3-175B stage shape (2 layers, hidden
-    12288, 96 heads, L = 2048, 8 x 256 slices): sampled output rows against the
-    row-sampling oracle within 1e-4, so the bf16 path's larger error at this size
-    is its rounding, not the algorithm."""
-    from paper_2102_07988_amd import terapipe as tp
-    n_layers, H, heads, L, n = 2, 12288, 96, 2048, 256
-    print(f"case fp32 validation: H={H} heads={heads} L={L} 8x{n} forward", flush=True)
-    dev = torch.device("cuda:0")
-    params = synth.stage_params(n_layers, H, seed=synth.SEED_PARAMS, dtype=torch.float32,
-                                device=dev)
-    x = synth.hidden_states(L, H, seed=synth.SEED_X, dtype=torch.float32, device=dev)
-    st = tp.Stage(params, H, heads, L, dtype="fp32", wgrad="deferred")
-    y = torch.empty_like(x)
-    for l in range(0, L, n):
-        st.forward(l, l + n, x[l:l + n], out=y[l:l + n])
-    torch.cuda.synchronize()
-    del st
-    rows = [0, 7, n - 1, n, 1023, 1024, 1536, L - n, L - 1]
-    p64 = synth.params_f64([{k: v.cpu() for k, v in p.items()} for p in params])
-    del params
-    gc.collect()
-    y_rows = stage_output_rows(p64, synth.to_f64(x.cpu()), heads, rows)
-    err = rel_l2(y[rows].double().cpu().numpy(), y_rows)
-    print(f"  fp32 y{rows} vs row oracle: {err:.2e}", flush=True)
-    assert err < 1e-4
