@@ -155,6 +155,21 @@ tp_status tp_kv_prefix_reset(tp_stage *stage);
  * must be 16-byte aligned (else TP_ERR_INVALID). */
 tp_status tp_slice_forward(tp_stage *stage, int l, int r, const void *x, void *y);
 
+/* For callers that cannot allocate (code under stream capture, serving loops,
+ * harnesses that forbid allocation): tp_slice_forward with the partial sums of
+ * its kernels (split-K GEMM partials, key-split attention partials) in the
+ * library's static per-device scratch array of 32 MiB instead of the stage
+ * workspace.  Nothing is allocated: no device or host memory, no events (kernel
+ * timing is not recorded for this call).  The kernels and their split plans are
+ * those tp_slice_forward would use, so the results are the same.  The plan is
+ * made on the host first: a slice whose largest partial-sum buffer exceeds
+ * 32 MiB is rejected with TP_ERR_WORKSPACE and the stage left unchanged.  The
+ * array keeps whatever the last call left in it (no contents carry meaning
+ * across calls); calls that overlap on one device race on it, as do
+ * overlapping calls of different stages on one device.  Other arguments,
+ * checks and effects as tp_slice_forward. */
+tp_status tp_slice_forward_static(tp_stage *stage, int l, int r, const void *x, void *y);
+
 /* Backward of token slice [l, r) through every layer, in reverse layer order.
  * The backward pass of a cell runs over the slices in the reverse of their
  * forward order (the last paragraph of Sec. 3.3 applies the same slicing

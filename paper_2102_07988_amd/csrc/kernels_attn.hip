@@ -846,6 +846,10 @@ hipError_t fwd_d(const AttnArgs& a, hipStream_t s) {
   constexpr size_t lds = 2 * 2 * 64 * D * 2;
   AttnArgs b = a;
   plan_split(b, true);
+  if (a.need) {
+    *a.need = b.nsplit > 1 ? (long)b.nsplit * ((long)n * a.bs * a.H + 2L * a.bs * a.heads * n) : 0;
+    return hipSuccess;
+  }
   if (b.nsplit == 1) {
     hipError_t e = set_lds(attn_fwd_mfma<D, NWF, false, F16>, lds);
     if (e != hipSuccess) return e;
@@ -870,6 +874,10 @@ hipError_t dq_d(const AttnArgs& a, hipStream_t s) {
   constexpr size_t lds_q = 2 * 2 * 64 * D * 2;
   AttnArgs b = a;
   plan_split(b, false);
+  if (a.need) {
+    *a.need = b.nsplit > 1 ? (long)b.nsplit * n * a.bs * a.H : 0;
+    return hipSuccess;
+  }
   if (b.nsplit == 1) {
     e = set_lds(attn_bwd_dq_mfma<D, NWF, false, F16>, lds_q);
     if (e != hipSuccess) return e;
@@ -890,6 +898,7 @@ hipError_t dq_d(const AttnArgs& a, hipStream_t s) {
 template <int D, bool F16>
 hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
   const int n = a.r - a.l;
+  if (a.need) return dq_d<D, F16>(a, s);  // only the dQ kernel takes split scratch
   attn_bwd_rowdot<D><<<dim3(cdiv((long)n * a.heads, 4), 1, a.bs), 256, 0, s>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -346,6 +346,10 @@ hipError_t run_cfg(GemmArgs a, hipStream_t s) {
     while (splits > 1 && (a.K / splits < 8 * BK || (long)splits * a.M * a.N > a.ws_elems))
       --splits;
   }
+  if (a.need) {
+    *a.need = splits > 1 ? (long)cdiv(a.K, cdiv(cdiv(a.K, splits), BK) * BK) * a.M * a.N : 0;
+    return hipSuccess;
+  }
   if (splits > 1) {
     a.k_split = cdiv(cdiv(a.K, splits), BK) * BK;
     a.splits = cdiv(a.K, a.k_split);

@@ -588,6 +588,10 @@ hipError_t run_dma(GemmArgs a, hipStream_t s, int force_splits = 0) {
       }
     }
   }
+  if (a.need) {
+    *a.need = splits > 1 ? (long)cdiv(a.K, cdiv(nkt, splits) * BK) * a.M * a.N : 0;
+    return hipSuccess;
+  }
   if (splits > 1) {
     a.k_split = cdiv(nkt, splits) * BK;
     a.splits = cdiv(a.K, a.k_split);

@@ -72,7 +72,7 @@ __global__ __launch_bounds__(256) void gemm_generic_kernel(GemmArgs a) {
 
 template <typename T>
 static hipError_t gemm_generic_t(const GemmArgs& a, hipStream_t s) {
-  if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  if (a.need || a.M <= 0 || a.N <= 0) return hipSuccess;  // no scratch
   dim3 grid(cdiv(a.N, 64), cdiv(a.M, 64));
   switch (a.epi) {
     case EPI_STORE: gemm_generic_kernel<T, EPI_STORE><<<grid, 256, 0, s>>>(a); break;
@@ -179,6 +179,7 @@ __global__ __launch_bounds__(256) void attn_bwd_generic_kernel(AttnArgs a0) {
 
 template <typename T>
 static hipError_t attn_generic_t(const AttnArgs& a, bool bwd, hipStream_t s) {
+  if (a.need) return hipSuccess;  // no scratch
   const size_t lds = bwd ? (2 * (size_t)a.Lmax + 256 + 16) * 4 : ((size_t)a.Lmax + 128 + 16) * 4;
   if (lds > 160 * 1024) return hipErrorInvalidValue;
   if (lds > 64 * 1024) {

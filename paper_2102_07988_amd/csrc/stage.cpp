@@ -16,6 +16,10 @@
 
 using namespace tp;
 
+namespace tp {
+void* static_scratch(size_t* bytes);  // static_scratch.hip
+}
+
 namespace {
 
 struct LayerBufs {
@@ -83,6 +87,10 @@ struct tp_stage {
   hipStream_t stream;
   int cached_len = 0, bwd_frontier = 0;
   bool profiling = false;
+  // planning pass (tp_slice_forward_static): no launch, only the largest
+  // partial-sum scratch (fp32 elements) the slice's kernels would take
+  bool dry = false;
+  long dry_need = 0;
   // timing
   bool timing = false;
   std::vector<PendingTiming> pending;
@@ -214,6 +222,7 @@ hipEvent_t get_event(tp_stage* S) {
 // fails the launch (its status is returned; the events go back to the pool).
 template <typename Fn>
 hipError_t launch(tp_stage* S, int cls, double flops, double bytes, Fn&& fn) {
+  if (S->dry) return hipSuccess;
   if (!S->timing) return fn();
   hipEvent_t a = get_event(S);
   if (!a) return hipErrorOutOfMemory;
@@ -253,6 +262,13 @@ double gemm_bytes(const GemmArgs& g, size_t esz) {
 hipError_t run_gemm(tp_stage* S, int cls, GemmArgs g) {
   g.ws = S->sc.splitk;
   g.ws_elems = (long)S->sc.splitk_elems;
+  if (S->dry) {
+    long need = 0;
+    g.need = &need;
+    const hipError_t e = gemm(S->dt, g, S->stream);
+    S->dry_need = std::max(S->dry_need, need);
+    return e;
+  }
   return launch(S, cls, 2.0 * g.M * g.N * g.K, gemm_bytes(g, S->esz),
                 [&] { return gemm(S->dt, g, S->stream); });
 }
@@ -374,6 +390,13 @@ tp_status forward_impl(tp_stage* S, int l, int r, const void* x, void* y) {
     a.scale = 1.f / std::sqrt((float)S->d);
     a.q = rowp(B.q, lr, A, e), a.kc = B.kc, a.vc = B.vc, a.o = rowp(B.o, lr, A, e), a.lse = B.lse;
     a.f16 = mx;
+    if (S->dry) {
+      long need = 0;
+      a.need = &need;
+      TRY(attn_fwd(dt, a, st));
+      S->dry_need = std::max(S->dry_need, need);
+      a.need = nullptr;
+    }
     const double pairs = ((double)ntok * l + (double)ntok * (ntok + 1) / 2) * S->bsz;
     TRY(launch(S, K_ATTN_FWD, 4.0 * A * pairs, (2.0 * ntok + 2.0 * r) * S->bsz * A * e,
                [&] { return attn_fwd(dt, a, st); }));
@@ -589,6 +612,40 @@ tp_status tp_slice_forward(tp_stage* S, int l, int r, const void* x, void* y) {
   // (frontier below the cached length) only tp_kv_prefix_reset starts over
   if (l != S->cached_len || S->bwd_frontier != S->cached_len) return TP_ERR_ORDER;
   tp_status s = forward_impl(S, l, r, x, y);
+  if (s != TP_OK) return s;
+  S->cached_len = r;
+  S->bwd_frontier = r;
+  return TP_OK;
+}
+
+tp_status tp_slice_forward_static(tp_stage* S, int l, int r, const void* x, void* y) {
+  if (!S || !x || !y || !aligned16(x) || !aligned16(y)) return TP_ERR_INVALID;
+  if (l < 0 || r <= l || r > S->L) return TP_ERR_INVALID;
+  if (l != S->cached_len || S->bwd_frontier != S->cached_len) return TP_ERR_ORDER;
+  // plan the slice exactly as tp_slice_forward would run it (same split
+  // choices), nothing enqueued: the largest partial-sum scratch any of its
+  // kernels takes must fit the static array
+  S->dry = true;
+  S->dry_need = 0;
+  tp_status s = forward_impl(S, l, r, x, y);
+  S->dry = false;
+  if (s != TP_OK) return s;
+  size_t cap = 0;
+  void* p = static_scratch(&cap);
+  if ((size_t)S->dry_need * 4 > cap) return TP_ERR_WORKSPACE;
+  if (!p) return TP_ERR_HIP;
+  // the kernels, split plans included, are those of tp_slice_forward; only the
+  // partial sums live in the static array (one launch's partials at a time:
+  // every split product is reduced before the next launch on the stream).
+  // Timing events are not created here.
+  Scratch saved = S->sc;
+  const bool was_timing = S->timing;
+  S->sc.splitk = (float*)p;
+  S->sc.attn = (float*)p;
+  S->timing = false;
+  s = forward_impl(S, l, r, x, y);
+  S->sc = saved;
+  S->timing = was_timing;
   if (s != TP_OK) return s;
   S->cached_len = r;
   S->bwd_frontier = r;

@@ -53,6 +53,10 @@ struct GemmArgs {
   int k_split = 0, splits = 1;
   // set by the launcher: output-tile order (0 grid order, 1 XCD super-tiles)
   int walk = 0;
+  // Host-side planning: when set, the launcher launches nothing and stores
+  // the fp32 scratch elements (split-K partials) its plan for this product
+  // takes, 0 without a split.  The caller zeroes *need first.
+  long* need = nullptr;
 };
 
 hipError_t gemm(int dtype, const GemmArgs& a, hipStream_t s);
@@ -101,6 +105,9 @@ struct AttnArgs {
   // products of the backward on fp16 dS.  The backward's vc is bf16 (dP = dO
   // V^T and dV = P^T dO keep the gradient side in bf16).
   int f16 = 0;
+  // Host-side planning, as GemmArgs::need: the key-split partials' fp32
+  // elements (forward: with the running maxima and sums), 0 without a split.
+  long* need = nullptr;
 };
 // The arguments of sequence blockIdx.z of the batch as a one-sequence view:
 // pointers moved to its columns (element type T) and planes; the row stride

@@ -28,7 +28,8 @@ SYNTH_NAMES = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
                "ln2_g", "ln2_b", "w1", "b1", "w2", "b2")
 
 EXPORTED = ("tp_stage_workspace_bytes", "tp_stage_init", "tp_stage_destroy",
-            "tp_kv_prefix_reset", "tp_slice_forward", "tp_slice_backward",
+            "tp_kv_prefix_reset", "tp_slice_forward", "tp_slice_forward_static",
+            "tp_slice_backward",
             "tp_profile_slice_cost", "tp_dp_optimal_slicing", "tp_dp_batch_split",
             "tp_dp_joint_slicing", "tp_fit_ctx_model",
             "tp_cost_table_from_model", "tp_profile_cost_model", "tp_status_string",
@@ -73,7 +74,7 @@ def _load():
     lib.tp_stage_destroy.argtypes = [vp]
     lib.tp_kv_prefix_reset.restype = ctypes.c_int
     lib.tp_kv_prefix_reset.argtypes = [vp]
-    for f in (lib.tp_slice_forward, lib.tp_slice_backward):
+    for f in (lib.tp_slice_forward, lib.tp_slice_forward_static, lib.tp_slice_backward):
         f.restype = ctypes.c_int
         f.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, vp]
     lib.tp_profile_slice_cost.restype = ctypes.c_int
@@ -218,6 +219,15 @@ class Stage:
         y = torch.empty_like(x) if out is None else out
         _check(lib.tp_slice_forward(self._h, l, r, x.data_ptr(), y.data_ptr()),
                f"tp_slice_forward [{l},{r})")
+        return y
+
+    def forward_static(self, l: int, r: int, x: torch.Tensor, out: Optional[torch.Tensor] = None):
+        """tp_slice_forward_static: the slice forward with its partial sums in the
+        library's static scratch (no allocation by the library)."""
+        x = self._io(x, r - l)
+        y = torch.empty_like(x) if out is None else out
+        _check(lib.tp_slice_forward_static(self._h, l, r, x.data_ptr(), y.data_ptr()),
+               f"tp_slice_forward_static [{l},{r})")
         return y
 
     def backward(self, l: int, r: int, dy: torch.Tensor, out: Optional[torch.Tensor] = None):

@@ -183,3 +183,20 @@ def test_dp_rejects_bad_arguments():
         tp.dp_optimal_slicing(bad, 16, 2)
     with pytest.raises(tp.TerapipeError):
         tp.dp_optimal_slicing(cost, 16, 2, -1)
+
+
+def test_static_forward_plans_on_the_host():
+    """tp_slice_forward_static plans the slice on the host: a slice whose
+    partial sums exceed the static scratch array (here the split output
+    projection of a 5120-wide layer over 256 rows) is rejected with
+    TP_ERR_WORKSPACE before anything is enqueued, and the order checks of
+    tp_slice_forward apply."""
+    X, Y = 0x7e0000000000, 0x7e0000100000
+    f = tp.lib.tp_slice_forward_static
+    rc, h = _init(tp.make_config(1, 5120, 40, 256, "bf16", "deferred"))
+    assert rc == tp.TP_OK
+    assert f(h, 0, 256, X, Y) == tp.TP_ERR_WORKSPACE
+    assert f(h, 8, 16, X, Y) == tp.TP_ERR_ORDER      # still at the sequence start
+    assert f(h, 0, 257, X, Y) == tp.TP_ERR_INVALID
+    assert f(h, 0, 8, None, Y) == tp.TP_ERR_INVALID
+    tp.lib.tp_stage_destroy(h)
