@@ -206,19 +206,22 @@ def test_profiler_table_and_dp_match_oracle():
 
 
 def test_profile_cost_model_mode():
-    """Model-mode profiling (Eq. 9): the table has the measured-table layout,
-    its j = 0 column is positive, and the model's predictions at the subset
-    points it was fitted on stay close to the costs measured again there (the
-    fit is a least-squares fit to those very points, so only timing noise and
-    model error separate them)."""
+    """Model-mode profiling (Eq. 9) on a 2-layer stage of the 1.3B width (hidden
+    2048, 16 heads, 1024 tokens, 64-token grid): the table has the
+    measured-table layout, its j = 0 column is positive and it is rebuilt
+    exactly from that column and the coefficients.  The full table is then
+    measured twice; on the points the model did not measure, its cost error
+    against the first measurement must stay within three times the
+    repeat-measurement noise (the second measurement against the first) plus
+    one percent.  The overhead errors are printed next to their noise."""
     from paper_2102_07988_amd import terapipe as tp
-    H, heads, L, unit = 512, 4, 512, 32
+    H, heads, L, unit = 2048, 16, 1024, 64
     params, _, _ = make_inputs(2, H, L, "bf16", (4, 5, 6))
     dparams = [{k: v.cuda() for k, v in p.items()} for p in params]
     st = tp.Stage(dparams, H, heads, L, dtype="bf16", wgrad="deferred")
     U = L // unit
-    sub_lens, sub_ctxs = [32, 128, 256, 384], [32, 128, 256, 448]
-    cost, coef = st.profile_model(L, unit, sub_lens, sub_ctxs, warmup=2, reps=5)
+    sub_lens, sub_ctxs = [64, 128, 256, 512, 768], [64, 128, 256, 512, 768]
+    cost, coef = st.profile_model(L, unit, sub_lens, sub_ctxs, warmup=3, reps=10)
     assert all(np.isfinite(coef))
     for k in range(1, U + 1):
         assert cost[k - 1, 0] > 0
@@ -228,17 +231,32 @@ def test_profile_cost_model_mode():
                 assert cost[k - 1, j] >= 0
     # the table rebuilt from its own j = 0 column and coefficients is identical
     assert np.array_equal(tp.cost_table_from_model(cost[:, 0], unit, coef), cost)
-    tf, tb = st.profile(sub_lens, sub_ctxs, warmup=2, reps=5)
-    errs = []
-    for a, i in enumerate(sub_lens):
-        for b, c in enumerate(sub_ctxs):
-            if i + c <= L:
-                errs.append(abs(cost[i // unit - 1, c // unit] - (tf[a, b] + tb[a, b]))
-                            / (tf[a, b] + tb[a, b]))
-    assert np.median(errs) < 0.25, errs
+    lens = [unit * k for k in range(1, U + 1)]
+    ctxs = [unit * j for j in range(U)]
+    tables = []
+    for _ in range(2):
+        tf, tb = st.profile(lens, ctxs, warmup=3, reps=10)
+        tables.append(np.where(tf >= 0, tf + tb, -1).astype(np.int64))
+    A, B = tables
+    sub = {(i // unit, c // unit) for i in sub_lens for c in sub_ctxs}
+    err, noise, ov_err, ov_noise = [], [], [], []
+    for k in range(1, U + 1):
+        for j in range(1, U - k + 1):
+            if (k, j) in sub:
+                continue
+            err.append(abs(cost[k - 1, j] - A[k - 1, j]) / A[k - 1, j])
+            noise.append(abs(B[k - 1, j] - A[k - 1, j]) / A[k - 1, j])
+            ov, ov_b = A[k - 1, j] - A[k - 1, 0], B[k - 1, j] - B[k - 1, 0]
+            if ov > 0:
+                ov_err.append(abs(cost[k - 1, j] - cost[k - 1, 0] - ov) / ov)
+                ov_noise.append(abs(ov_b - ov) / ov)
+    print(f"held-out points {len(err)}: cost error median {np.median(err):.4f} "
+          f"(repeat noise {np.median(noise):.4f}); overhead error median "
+          f"{np.median(ov_err):.4f} (repeat noise {np.median(ov_noise):.4f})", flush=True)
+    assert np.median(err) <= 3 * np.median(noise) + 0.01, (np.median(err), np.median(noise))
     # the DP runs on the model table
-    lens, T = tp.dp_optimal_slicing(cost, unit, 8)
-    assert sum(lens) == L and T > 0
+    lens_dp, T = tp.dp_optimal_slicing(cost, unit, 8)
+    assert sum(lens_dp) == L and T > 0
 
 
 def test_mfma_peak_probe_plausible():
