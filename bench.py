@@ -80,29 +80,49 @@ def parse_slicing(s: str, L: int, default):
 
 
 def cpu_baseline(params0, x, dy, hidden: int, heads: int, n_tokens: int, op_parts: int = 1):
-    """Time the fp64 oracle (all host threads) on one layer of the workload
-    (the benchmark's own layer-0 parameters) over one slice of the first
-    n_tokens tokens after no context: forward + backward."""
+    """Time the fp64 oracle on one layer of the workload (the benchmark's own
+    layer-0 parameters): forward + backward of one slice of the first n tokens
+    after no context, for n = 16 and n = n_tokens on all host threads, and for
+    n = 4 on one thread.  `value` is the all-thread rate at n = n_tokens; every
+    point is listed."""
+    import ctypes
     import numpy as np
     import torch
 
     from oracle import OracleStage, slice_flops
 
     p64 = {k: v.detach().to("cpu").to(torch.float64).numpy() for k, v in params0.items()}
-    x64 = x[:n_tokens].to("cpu").to(torch.float64).numpy()
-    dy64 = dy[:n_tokens].to("cpu").to(torch.float64).numpy()
-    st = OracleStage([p64], hidden, heads, n_tokens, op_parts=op_parts)
-    del p64
-    t0 = time.perf_counter()
-    st.run_sequence(x64, dy64, [n_tokens])
-    dt = time.perf_counter() - t0
-    flops = slice_flops(n_tokens, 0, hidden) // op_parts
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "seconds": round(dt, 3),
+    try:
+        gomp = ctypes.CDLL("libgomp.so.1")
+    except OSError:
+        gomp = None
+
+    def point(n, nthreads):
+        x64 = x[:n].to("cpu").to(torch.float64).numpy()
+        dy64 = dy[:n].to("cpu").to(torch.float64).numpy()
+        st = OracleStage([p64], hidden, heads, n, op_parts=op_parts)
+        if gomp is not None:
+            gomp.omp_set_num_threads(nthreads)
+        t0 = time.perf_counter()
+        st.run_sequence(x64, dy64, [n])
+        dt = time.perf_counter() - t0
+        if gomp is not None:
+            gomp.omp_set_num_threads(threads)
+        fl = slice_flops(n, 0, hidden) // op_parts
+        return {"len": n, "ctx": 0, "threads": nthreads if gomp is not None else threads,
+                "seconds": round(dt, 3), "tflops": fl / dt / 1e12}
+
+    pts = [point(16, threads), point(n_tokens, threads)]
+    if gomp is not None:
+        pts.append(point(4, 1))
+    main = pts[1]
+    return {"value": main["tflops"], "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "seconds": main["seconds"], "points": pts,
             "sample": f"1 layer of the same shape (H={hidden}, {heads // op_parts} of {heads} "
                       f"heads), one slice of {n_tokens} tokens at context 0, forward+backward, "
-                      f"fp64"}
+                      f"fp64, {threads} threads (points: 16 tokens on {threads} threads, 4 tokens "
+                      f"on 1 thread)"}
 
 
 def _subset(U: int):
