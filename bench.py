@@ -50,7 +50,7 @@ PEAK_HBM_GBS = 8000.0
 TRAFFIC = {
     "gemm_bwd_dw_tn": {"workload": "gpt3-175b-stage",
                        "source": "paper_2102_07988_amd/csrc/kernels_gemm_dma.hip",
-                       "sha256_16": "4da15140a3bd24c0", "bytes_per_launch": 6605440564},
+                       "sha256_16": "0c9119a7a0d01de0", "bytes_per_launch": 6603684408},
 }
 
 
