@@ -22,6 +22,11 @@ more), unsplit d = 128 dQ launches.
   gradients with 4 x 512 backward slices.
 * One GPU's shard of the paper's 175B settings with operation partitioning
   (Table 1 settings (10) and (9)): 8-way (2 layers) and 4-way (1 layer).
+* The largest shapes the stage accepts: hidden 16384 (128 heads, one layer,
+  256 tokens in ragged slices), and the longest sequence, 20344 tokens (the
+  generic attention's one-row-per-block LDS limit; hidden 256, 2 heads of
+  128), in ragged slices of up to 8192 tokens and a short last slice after
+  a 20000-token prefix.
 
 Tolerance: rel-L2 2e-2 per tensor in bf16 (y, dx and each of the 12
 parameter gradients of every layer), 1e-4 in the fp32 validation mode.
@@ -157,3 +162,29 @@ def test_175b_operation_partitioning_shard_full_sequence(n_layers, parts):
     ref = oracle(params, x, dy, heads // parts)
     check_run(ref, params, x, dy, H, heads, L, "bf16", [256] * 8, None, "deferred",
               f"175B {parts}-way shard, {n_layers} layer(s)", op_parts=parts)
+
+
+def test_maximum_hidden_size():
+    """Hidden size 16384 (the LayerNorm kernels' register limit), 128 heads of
+    128, one layer; ragged forward and backward slicings, both weight-gradient
+    modes."""
+    H, heads, L = 16384, 128, 256
+    params, x, dy = inputs(1, H, L, "bf16")
+    ref = oracle(params, x, dy, heads)
+    check_run(ref, params, x, dy, H, heads, L, "bf16", [100, 156], [200, 56], "per_slice",
+              "hidden 16384, per-slice dW")
+    check_run(ref, params, x, dy, H, heads, L, "bf16", [100, 156], None, "deferred",
+              "hidden 16384, deferred dW")
+
+
+def test_maximum_sequence_length():
+    """The longest sequence a stage accepts, 20344 tokens, at hidden 256 (2 heads
+    of 128): slices of 8192 tokens and a ragged tail, and a 344-token slice
+    after a 20000-token prefix."""
+    H, heads, L = 256, 2, 20344
+    params, x, dy = inputs(1, H, L, "bf16")
+    ref = oracle(params, x, dy, heads)
+    check_run(ref, params, x, dy, H, heads, L, "bf16", [8192, 8192, 3960], [5000, 15344],
+              "per_slice", "20344 tokens, per-slice dW")
+    check_run(ref, params, x, dy, H, heads, L, "bf16", [20000, 344], None, "deferred",
+              "20344 tokens, short slice after a 20000-token prefix")
