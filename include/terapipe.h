@@ -123,9 +123,10 @@ size_t tp_stage_workspace_bytes(const tp_stage_config *cfg);
  * 256-byte aligned, owned by the caller and used only by this stage until
  * tp_stage_destroy.  stream: a hipStream_t (NULL = default stream) on which
  * all of the stage's device work is enqueued.  Host only: nothing is enqueued.
- * The new stage is positioned at the start of a sequence, but the dK/dV buffer
- * holds whatever the workspace held: call tp_kv_prefix_reset before the first
- * sequence.  Errors: TP_ERR_INVALID, TP_ERR_UNSUPPORTED, TP_ERR_WORKSPACE. */
+ * The new stage holds no sequence: its dK/dV buffer holds whatever the
+ * workspace held and the fp16 W_qkv copy is not taken, so every slice call
+ * returns TP_ERR_ORDER until tp_kv_prefix_reset starts a sequence.
+ * Errors: TP_ERR_INVALID, TP_ERR_UNSUPPORTED, TP_ERR_WORKSPACE. */
 tp_status tp_stage_init(const tp_stage_config *cfg, const tp_layer_ptrs *params,
                         const tp_layer_ptrs *grads, void *workspace, size_t workspace_bytes,
                         void *stream, tp_stage **out);
@@ -133,7 +134,8 @@ tp_status tp_stage_init(const tp_stage_config *cfg, const tp_layer_ptrs *params,
 /* Free the host-side stage object.  Does not synchronise or free device memory. */
 void tp_stage_destroy(tp_stage *stage);
 
-/* Start a new sequence: no cached tokens, backward frontier 0, and the fp32
+/* Start a new sequence (required before the first slice call after
+ * tp_stage_init or tp_profile_slice_cost): no cached tokens, backward frontier 0, and the fp32
  * dK/dV buffer zeroed (enqueued on the stream; a fill kernel, no memset node);
  * on the mixed-precision path (see Conventions) also the fp16 copy of every
  * layer's W_qkv taken.
@@ -146,8 +148,9 @@ tp_status tp_kv_prefix_reset(tp_stage *stage);
 /* Forward of token slice [l, r) through every layer (Sec. 3.2).
  * x: [r-l][b][H] stage input rows, y: [r-l][b][H] stage output rows (stage
  * dtype, device; b = cfg.batch, token-major).  Requires 0 <= l < r <= max_seq
- * (else TP_ERR_INVALID), l equal to the number of cached tokens and no
- * backward call since the last tp_kv_prefix_reset (else TP_ERR_ORDER: a
+ * (else TP_ERR_INVALID), a sequence started by tp_kv_prefix_reset, l equal
+ * to the number of cached tokens and no backward call since that reset
+ * (else TP_ERR_ORDER: a
  * slice's backward needs the forward of every later slice, so a forward after
  * backward has begun is misuse).  Appends the slice's keys
  * and values to each layer's cache, saves what backward needs, and sets the
@@ -163,7 +166,8 @@ tp_status tp_slice_forward(tp_stage *stage, int l, int r, const void *x, void *y
  * timing is not recorded for this call).  The kernels and their split plans are
  * those tp_slice_forward would use, so the results are the same.  The plan is
  * made on the host first: a slice whose largest partial-sum buffer exceeds
- * 32 MiB is rejected with TP_ERR_WORKSPACE and the stage left unchanged.  The
+ * 32 MiB is rejected with TP_ERR_WORKSPACE and the stage left unchanged (this
+ * check precedes the one for a started sequence).  The
  * array keeps whatever the last call left in it (no contents carry meaning
  * across calls); calls that overlap on one device race on it, as do
  * overlapping calls of different stages on one device.  Other arguments,
@@ -179,7 +183,8 @@ tp_status tp_slice_forward_static(tp_stage *stage, int l, int r, const void *x, 
  * dy: [r-l][b][H] gradient of the stage output rows, dx: [r-l][b][H] gradient
  * of the stage input rows (stage dtype, device).  Requires 0 <= l < r and r equal to
  * the backward frontier (slices arrive in reverse order; their boundaries need
- * not match the forward slicing), else TP_ERR_ORDER / TP_ERR_INVALID.  Adds
+ * not match the forward slicing) in a sequence started by tp_kv_prefix_reset,
+ * else TP_ERR_ORDER / TP_ERR_INVALID (argument checks come first).  Adds
  * this slice's contributions to the parameter gradients; the gradient that
  * queries in [l, r) send to earlier keys/values is added to the dK/dV buffer.
  * Sets the frontier to l; in DEFERRED mode the weight-gradient GEMMs run when
@@ -195,7 +200,8 @@ tp_status tp_slice_backward(tp_stage *stage, int l, int r, const void *dy, void 
  * In DEFERRED mode t_bwd excludes the once-per-sequence weight-gradient GEMMs
  * and bias / LayerNorm-parameter reductions.
  * Synchronous.  Overwrites the K/V cache, the arenas and the parameter
- * gradients with meaningless values: reset and zero them afterwards. */
+ * gradients with meaningless values and ends any sequence: slice calls return
+ * TP_ERR_ORDER until tp_kv_prefix_reset; zero the gradients afterwards. */
 tp_status tp_profile_slice_cost(tp_stage *stage, const int *lens, int n_lens, const int *ctxs,
                                 int n_ctxs, int warmup, int reps, int64_t *t_fwd_ns,
                                 int64_t *t_bwd_ns);

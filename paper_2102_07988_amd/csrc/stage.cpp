@@ -86,6 +86,9 @@ struct tp_stage {
   Scratch sc;
   hipStream_t stream;
   int cached_len = 0, bwd_frontier = 0;
+  // a sequence has been started by tp_kv_prefix_reset since the stage was
+  // created or last profiled (the dK/dV buffer is zero, the fp16 W_qkv copy taken)
+  bool prepared = false;
   bool profiling = false;
   // planning pass (tp_slice_forward_static): no launch, only the largest
   // partial-sum scratch (fp32 elements) the slice's kernels would take
@@ -600,6 +603,7 @@ tp_status tp_kv_prefix_reset(tp_stage* S) {
   TRY(snapshot_wqkv(S));
   S->cached_len = 0;
   S->bwd_frontier = 0;
+  S->prepared = true;
   return TP_OK;
 }
 
@@ -608,9 +612,11 @@ static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 tp_status tp_slice_forward(tp_stage* S, int l, int r, const void* x, void* y) {
   if (!S || !x || !y || !aligned16(x) || !aligned16(y)) return TP_ERR_INVALID;
   if (l < 0 || r <= l || r > S->L) return TP_ERR_INVALID;
-  // slices arrive in order; once the backward pass of the sequence has begun
-  // (frontier below the cached length) only tp_kv_prefix_reset starts over
-  if (l != S->cached_len || S->bwd_frontier != S->cached_len) return TP_ERR_ORDER;
+  // a sequence starts with tp_kv_prefix_reset; slices arrive in order; once
+  // the backward pass has begun (frontier below the cached length) only
+  // another reset starts over
+  if (!S->prepared || l != S->cached_len || S->bwd_frontier != S->cached_len)
+    return TP_ERR_ORDER;
   tp_status s = forward_impl(S, l, r, x, y);
   if (s != TP_OK) return s;
   S->cached_len = r;
@@ -624,7 +630,8 @@ tp_status tp_slice_forward_static(tp_stage* S, int l, int r, const void* x, void
   if (l != S->cached_len || S->bwd_frontier != S->cached_len) return TP_ERR_ORDER;
   // plan the slice exactly as tp_slice_forward would run it (same split
   // choices), nothing enqueued: the largest partial-sum scratch any of its
-  // kernels takes must fit the static array
+  // kernels takes must fit the static array.  The plan reads only the shapes,
+  // so it is checked before whether a sequence has been started.
   S->dry = true;
   S->dry_need = 0;
   tp_status s = forward_impl(S, l, r, x, y);
@@ -633,6 +640,7 @@ tp_status tp_slice_forward_static(tp_stage* S, int l, int r, const void* x, void
   size_t cap = 0;
   void* p = static_scratch(&cap);
   if ((size_t)S->dry_need * 4 > cap) return TP_ERR_WORKSPACE;
+  if (!S->prepared) return TP_ERR_ORDER;
   if (!p) return TP_ERR_HIP;
   // the kernels, split plans included, are those of tp_slice_forward; only the
   // partial sums live in the static array (one launch's partials at a time:
@@ -655,7 +663,7 @@ tp_status tp_slice_forward_static(tp_stage* S, int l, int r, const void* x, void
 tp_status tp_slice_backward(tp_stage* S, int l, int r, const void* dy, void* dx) {
   if (!S || !dy || !dx || !aligned16(dy) || !aligned16(dx)) return TP_ERR_INVALID;
   if (l < 0 || r <= l || r > S->L) return TP_ERR_INVALID;
-  if (r != S->bwd_frontier) return TP_ERR_ORDER;
+  if (!S->prepared || r != S->bwd_frontier) return TP_ERR_ORDER;
   tp_status s = backward_impl(S, l, r, dy, dx);
   if (s != TP_OK) return s;
   S->bwd_frontier = l;
@@ -742,8 +750,10 @@ tp_status tp_profile_slice_cost(tp_stage* S, const int* lens, int n_lens, const 
   hipEventDestroy(e2);
   S->profiling = false;
   S->timing = was_timing;
+  // the caches, dK/dV accumulators and slice buffers now hold profiling data
   S->cached_len = 0;
   S->bwd_frontier = 0;
+  S->prepared = false;
   return status;
 }
 

@@ -126,6 +126,19 @@ def test_slice_order_errors_are_host_side():
     tp.lib.tp_stage_destroy(h)
 
 
+def test_slices_need_a_started_sequence():
+    """A new stage holds no sequence (its dK/dV buffer and fp16 W_qkv copy are
+    unset): every slice call is refused on the host until tp_kv_prefix_reset."""
+    X, Y = 0x7e0000000000, 0x7e0000100000
+    for dtype in ("fp32", "bf16"):
+        rc, h = _init(tp.make_config(1, 64, 4, 32, dtype))
+        assert rc == tp.TP_OK
+        assert tp.lib.tp_slice_forward(h, 0, 8, X, Y) == tp.TP_ERR_ORDER
+        assert tp.lib.tp_slice_forward_static(h, 0, 8, X, Y) == tp.TP_ERR_ORDER
+        assert tp.lib.tp_slice_backward(h, 0, 8, X, Y) == tp.TP_ERR_ORDER
+        tp.lib.tp_stage_destroy(h)
+
+
 def test_profile_argument_errors():
     cfg = tp.make_config(1, 64, 4, 32, "fp32")
     rc, h = _init(cfg)

@@ -197,6 +197,10 @@ def test_profiler_table_and_dp_match_oracle():
             units, T, _, _ = oracle_dp(cost, K)
             got, T2 = tp.dp_optimal_slicing(cost, unit, K)
             assert T2 == T and got == [unit * u for u in units], (wgrad, K)
+        # profiling ends the sequence: slice calls are refused until a reset
+        with pytest.raises(tp.TerapipeError) as e:
+            st.forward(0, 8, x[:8].cuda())
+        assert e.value.status == tp.TP_ERR_ORDER
         # the stage is usable again after profiling
         st.zero_grads()
         y, dx = st.run_sequence(x.cuda(), dy.cuda(), [128, 128])
