@@ -22,6 +22,9 @@
 //             fp32 dK/dV buffer (each element owned by one lane: no atomics).
 //  dQ       : one block of 32 queries per wave; S^T = K Q^T, dP^T = V dO^T,
 //             dQ^T += K^T dS^T.
+//  stored dS: the dK kernel also writes dS of every (key, query) block it
+//             forms; dQ^T += K^T dS^T then streams it instead of forming the
+//             scores and dP once more.
 // K/V (or Q/dO) tiles move from HBM to a double-buffered LDS ring by the LDS
 // DMA, so the next tile streams in while the current one is multiplied.
 #include "tp_common.hpp"
@@ -196,6 +199,66 @@ struct Tile {
     }
   }
 };
+
+// DMA of a 64-key x (128 NS)-query tile of the stored dS (32-query blocks of
+// [key][32], qstride elements apart) into NS consecutive Tile<128> layouts
+// (row = key); per-thread chunk offsets computed once; a tile with fewer valid
+// rows repeats row rvalid - 1.
+template <int NTH, int NS>
+struct DsDma {
+  static constexpr int ROWS = 64, CH = NS * ROWS * 16 / NTH;
+  static_assert(CH * NTH == NS * ROWS * 16, "uneven tile DMA");
+  uint32_t off[CH];
+  int w;  // wave index, wave-uniform
+  // slot sl of the tile: sub-tile sl / 1024, row and chunk within it
+  __device__ static long src(int sl, long qstride, int rvalid) {
+    const int t = sl >> 10, r = (sl >> 4) & 63, c = (sl & 15) ^ Tile<128>::f(r);
+    return (4 * t + (c >> 2)) * qstride + min(r, rvalid - 1) * 32 + (c & 3) * 8;
+  }
+  __device__ DsDma(long qstride, int wave) : w(wave) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < CH; ++i) off[i] = (uint32_t)(src(i * NTH + w * 64 + lane, qstride, ROWS) * 2);
+  }
+  // G: key 0 of the tile in the first query block
+  __device__ void issue(const uint16_t* G, long qstride, int rvalid, uint16_t* lds) const {
+    if (rvalid >= ROWS) {
+#pragma unroll
+      for (int i = 0; i < CH; ++i) dma16((const char*)G + off[i], lds + (i * NTH + w * 64) * 8);
+    } else {
+      const int lane = threadIdx.x & 63;
+#pragma unroll
+      for (int i = 0; i < CH; ++i)
+        dma16(G + src(i * NTH + w * 64 + lane, qstride, rvalid), lds + (i * NTH + w * 64) * 8);
+    }
+  }
+};
+
+// Tile<128>::col8 for a tile whose columns are stored with bits 2 and 3 of the
+// column index swapped (the stored dS): the 4-column blocks the transposing
+// reads fetch move as a whole, so each lane still receives column cb + lane % 32.
+__device__ inline u32x4 col8_swapped(uint32_t base, int r0, int cb, int lane) {
+  using T = Tile<128>;
+  const int g = lane >> 4, j = lane & 15;
+  const int col = cb + 16 * (g & 1) + 4 * (j & 3);
+  const int pc = (col & ~12) | ((col & 4) << 1) | ((col & 8) >> 1);
+  const int r = r0 + 4 * (g >> 1) + (j >> 2);
+  const uint32_t inchunk = (pc & 7) << 1;
+  return join(ds_read_tr(base + T::off(r, pc >> 3) + inchunk),
+              ds_read_tr(base + T::off(r + 8, pc >> 3) + inchunk));
+}
+
+// 16-bit operand values of keys >= r set to zero: slot e of group G stands for
+// key r0 + 4 G + e (e < 4) or r0 + 8 + 4 G + e - 4, two slots per register,
+// the lower one in the low half.
+__device__ inline u32x4 mask_keys(u32x4 x, int r0, int G, int r) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int k = r0 + (q < 2 ? 4 * G + 2 * q : 8 + 4 * G + 2 * (q - 2));
+    x[q] &= (k < r ? 0xffffu : 0u) | (k + 1 < r ? 0xffff0000u : 0u);
+  }
+  return x;
+}
 
 // ------------------------------------------------------------------ forward
 
@@ -389,19 +452,82 @@ __global__ __launch_bounds__(256) void attn_bwd_rowdot(AttnArgs a0) {
 
 // ------------------------------------------------------------ dK / dV
 
-// MODE 1: dV (S, P, dV += P^T dO); MODE 2: dK (S, dP, dS, dK += dS^T Q).
-// Each holds one accumulator set and fits two waves per SIMD; the pair
+// Wait until at most BASE + k * PER vector memory instructions are in flight,
+// k (wave-uniform, 0..KMAX) picking the immediate.
+template <int BASE, int PER, int KMAX>
+__device__ inline void wait_vm_stores(int k) {
+  if constexpr (KMAX == 0) {
+    wait_vm<BASE>();
+  } else {
+    if (k >= KMAX) wait_vm<BASE + KMAX * PER>();
+    else wait_vm_stores<BASE, PER, KMAX - 1>(k);
+  }
+}
+
+// Adds a wave's 32-key block of fp32 results, acc[j][v] * mul for key
+// s0 + 8 (v / 4) + 4 G + v % 4 and column 32 j + c, into the fp32 buffer buf
+// (this head's first column, rows of H); keys >= r are left out.  When all 32
+// keys exist, the loads of column block j + 1 are issued before block j is
+// added and stored, so the read latency is paid about once.
+template <int JB>
+__device__ inline void add_rows_f32(float* buf, const f32x16_t (&acc)[JB], float mul, int s0,
+                                    int r, int H, int G, int c) {
+  if (s0 + 32 <= r) {
+    float* b = buf + (long)s0 * H + c;
+    auto rowoff = [&](int v) { return (long)(8 * (v >> 2) + 4 * G + (v & 3)) * H; };
+    float cur[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) cur[v] = b[rowoff(v)];
+#pragma unroll
+    for (int j = 0; j < JB; ++j) {
+      float nx[16];
+      if (j + 1 < JB) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) nx[v] = b[rowoff(v) + 32 * (j + 1)];
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) b[rowoff(v) + 32 * j] = cur[v] + acc[j][v] * mul;
+      if (j + 1 < JB) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) cur[v] = nx[v];
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < JB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int key = s0 + 8 * (v >> 2) + 4 * G + (v & 3);
+        if (key < r) buf[(long)key * H + 32 * j + c] += acc[j][v] * mul;
+      }
+  }
+}
+
+// MODE 1: dV (S, P, dV += P^T dO); MODE 2: dK (S, dP, dS, dK += dS^T Q);
+// MODE 3: MODE 2 that also stores dS for the streaming dQ kernel.  Each holds
+// one accumulator set and fits two waves per SIMD; the MODE 1 + 2 pair
 // recomputes S once more than a kernel forming both would.
+//
+// Stored dS (MODE 3): one plane of pd_ld / 32 query blocks per sequence and
+// head; query block qb (queries l + 32 qb ...) holds r rows of 32 values, row
+// = key, at qb * r * 32 + key * 32, so a wave's stores of one block fill whole
+// contiguous lines and a reader's tile of consecutive keys is one contiguous
+// piece.  Values fp16 (F16) or bf16, as the dK product rounds them, in operand
+// order: query 16 h + 4 G + e + 8 u (e < 4) at column 16 h + 8 G + 4 u + e,
+// i.e. bits 2 and 3 of the query index swapped, so each lane stores the 8
+// values of a reduction half with one 16-byte store.  A (32-key, 32-query) block is written when its first key is below r
+// and not after the block's last query (masked entries as zeros), the same
+// condition under which the dQ kernel reads it.
 // ST query tiles form the LDS ring: tile qb + ST - 1 is requested while tile
 // qb is multiplied.
 // F16: q and k are fp16 (scores on fp16 operands; the dK kernel's dS product
 // on fp16 dS); v and the gradients stay bf16.
 template <int D, int NW, int MODE, int ST, bool F16>
 __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dkdv_mfma(AttnArgs a0) {
-  static_assert(MODE == 1 || MODE == 2, "dV (1) or dK (2)");
+  static_assert(MODE >= 1 && MODE <= 3, "dV (1), dK (2), dK storing dS (3)");
   const AttnArgs a = attn_seq_view<uint16_t>(a0);
   using T = Tile<D>;
-  constexpr bool DO_K = MODE == 2, DO_V = MODE == 1;
+  constexpr bool DO_K = MODE >= 2, DO_V = MODE == 1, STORE = MODE == 3;
   constexpr int NTH = 64 * NW, BQ = 32, KS = D / 16, JB = D / 32;
   constexpr int TILE = BQ * D;                           // elements
   constexpr int STAGE = 2 * TILE + NW * 128;             // Q, dO, then per-wave [lse | D]
@@ -421,7 +547,9 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dkdv_mfma(AttnArgs a0) {
   // K fragments of the wave's keys stay in registers; the dK kernel keeps
   // the block's V rows (needed for dP) in LDS, loaded once after the
   // query-tile ring, and reads them per query block
-  constexpr bool V_LDS = MODE == 2;
+  constexpr bool V_LDS = DO_K;
+  // this lane's row in query block 0 of the stored dS plane (MODE 3)
+  const long prow = STORE ? ((long)blockIdx.z * a.heads + h) * a.r * a.pd_ld + (long)s_me * 32 : 0;
   u32x4 kf[KS];
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) {
@@ -455,15 +583,33 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dkdv_mfma(AttnArgs a0) {
                                     smem + ST * STAGE);
     for (int i = 0; i < ST - 1 && i < nqb; ++i) issue(i, i);
   }
+  // MODE 3: a query block that takes part issues STORES store instructions,
+  // counted by vmcnt like the DMA; `recent` has bit j set when block qb - 1 - j
+  // did, so the stores of the ST - 1 blocks issued after tile qb's DMA may
+  // stay in flight while waiting for that tile
+  constexpr int STORES = 2;
+  unsigned recent = 0;
+  bool stored = false;
   for (int qb = 0; qb < nqb; ++qb) {
-    // tile qb has landed once at most the ST - 2 later tiles are in flight
-    if (qb + ST - 1 <= nqb) wait_vm<(ST - 2) * PER_ISSUE>();
-    else wait_vm<0>();
+    // tile qb has landed once at most the ST - 2 later tiles (and the stores
+    // issued after tile qb's DMA) are in flight
+    if (qb + ST - 1 <= nqb) {
+      if constexpr (STORE) {
+        recent = ((recent << 1) | (stored ? 1u : 0u)) & ((1u << (ST - 1)) - 1);
+        wait_vm_stores<(ST - 2) * PER_ISSUE, STORES, ST - 1>(__builtin_popcount(recent));
+      } else {
+        wait_vm<(ST - 2) * PER_ISSUE>();
+      }
+    } else {
+      if constexpr (STORE) recent = ((recent << 1) | (stored ? 1u : 0u)) & ((1u << (ST - 1)) - 1);
+      wait_vm<0>();
+    }
     __builtin_amdgcn_s_barrier();
     if (qb + ST - 1 < nqb) issue((qb + ST - 1) % ST, qb + ST - 1);
     const int i0 = i_begin + qb * BQ, qval = min(BQ, n - i0);
     // the wave's keys [s_w, s_w + 32) meet queries up to l + i0 + qval - 1
-    if (s_w <= a.l + i0 + qval - 1 && s_w < a.r) {
+    stored = s_w <= a.l + i0 + qval - 1 && s_w < a.r;
+    if (stored) {
       const uint32_t Qt = sbase + (qb % ST) * STAGE * 2, Ot = Qt + TILE * 2;
       // lse and D of this lane's 16 query rows: 4 consecutive rows per v / 4
       const uint32_t LD = Qt + 2 * TILE * 2 + w * 256;
@@ -551,6 +697,9 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dkdv_mfma(AttnArgs a0) {
         }
         if constexpr (DO_K) {
           const u32x4 db = acc_half<F16>(ds, ks);
+          if constexpr (STORE) {
+            if (s_me < a.r) *(u32x4*)(a.dst + prow + (long)(i0 >> 5) * a.r * 32 + 16 * ks + 8 * G) = db;
+          }
           u32x4 qb2[JB];
 #pragma unroll
           for (int j = 0; j < JB; ++j) qb2[j] = T::col8(Qt, 16 * ks, 32 * j, lane);
@@ -563,56 +712,9 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dkdv_mfma(AttnArgs a0) {
       }
     }
   }
-  // dk[j][v], dv[j][v]: key s_w + 8 (v / 4) + 4 G + v % 4, column 32 j + c.
-  // Added into the fp32 buffers; when all 32 keys of the wave exist, the loads
-  // of column block j + 1 are issued before block j is added and stored, so the
-  // read latency is paid about once.
-  if (s_w + 32 <= a.r) {
-    float* dkb = a.dk + (long)s_w * H + h * D + c;
-    float* dvb = a.dv + (long)s_w * H + h * D + c;
-    auto rowoff = [&](int v) { return (long)(8 * (v >> 2) + 4 * G + (v & 3)) * H; };
-    float ck[16], cv[16];
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      if constexpr (DO_K) ck[v] = dkb[rowoff(v)];
-      if constexpr (DO_V) cv[v] = dvb[rowoff(v)];
-    }
-#pragma unroll
-    for (int j = 0; j < JB; ++j) {
-      float nk[16], nv[16];
-      if (j + 1 < JB) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          if constexpr (DO_K) nk[v] = dkb[rowoff(v) + 32 * (j + 1)];
-          if constexpr (DO_V) nv[v] = dvb[rowoff(v) + 32 * (j + 1)];
-        }
-      }
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        if constexpr (DO_K) dkb[rowoff(v) + 32 * j] = ck[v] + dk[j][v] * a.scale;
-        if constexpr (DO_V) dvb[rowoff(v) + 32 * j] = cv[v] + dv[j][v];
-      }
-      if (j + 1 < JB) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          if constexpr (DO_K) ck[v] = nk[v];
-          if constexpr (DO_V) cv[v] = nv[v];
-        }
-      }
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < JB; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int key = s_w + 8 * (v >> 2) + 4 * G + (v & 3);
-        if (key < a.r) {
-          const long off = (long)key * H + h * D + 32 * j + c;
-          if constexpr (DO_K) a.dk[off] += dk[j][v] * a.scale;
-          if constexpr (DO_V) a.dv[off] += dv[j][v];
-        }
-      }
-  }
+  // dk[j][v], dv[j][v]: key s_w + 8 (v / 4) + 4 G + v % 4, column 32 j + c
+  if constexpr (DO_K) add_rows_f32<JB>(a.dk + h * D, dk, a.scale, s_w, a.r, H, G, c);
+  if constexpr (DO_V) add_rows_f32<JB>(a.dv + h * D, dv, 1.f, s_w, a.r, H, G, c);
 }
 
 // ------------------------------------------------------------------- dQ
@@ -751,6 +853,113 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_mfma(AttnArgs a0) {
             make_uint2(pack_bf16x2(dq[j][v] * a.scale, dq[j][v + 1] * a.scale),
                        pack_bf16x2(dq[j][v + 2] * a.scale, dq[j][v + 3] * a.scale));
       }
+  }
+}
+
+// ------------------------------------------------- dQ from the stored dS
+
+// dQ^T += K^T dS^T over the dS the dK kernel stored: per 64-key tile, the K
+// rows and the stored dS rows of the block's 32-query blocks (128 or 256
+// queries) move through an LDS ring; each wave owns QH blocks of 32 queries.
+// Rows of keys >= r (repeats in the last tile) are zeroed in the dS operand.
+template <int D, int NW, int QH, int ST, bool F16>
+__global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_stream(AttnArgs a0) {
+  const AttnArgs a = attn_seq_view<uint16_t>(a0);
+  using TK = Tile<D>;
+  constexpr int NTH = 64 * NW, BKV = 64, JB = D / 32, QB = 32 * QH * NW;
+  static_assert(QB == 128 || QB == 256, "128 or 256 query columns per block");
+  constexpr int TILE_K = BKV * D, STAGE = TILE_K + BKV * QB, NS = QB / 128;
+  static_assert((BKV * D / 8) % NTH == 0 && (BKV * QB / 8) % NTH == 0, "uneven tile DMA");
+  constexpr int PER_ISSUE = (BKV * D / 8) / NTH + (BKV * QB / 8) / NTH;
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+  const int h = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int G = lane >> 5, c = lane & 31, H = a.ld;  // H: row stride
+  const int i_lo = blockIdx.x * QB, q_lo = a.l + i_lo;
+  const long qstride = (long)a.r * 32;  // elements between query blocks
+  const uint16_t* Sp =
+      a.dst + ((long)blockIdx.z * a.heads + h) * a.r * a.pd_ld + (long)(i_lo >> 5) * qstride;
+  const uint16_t* Kc = (const uint16_t*)a.kc + h * D;
+  const int kend_blk = min(a.r, q_lo + QB);
+  const uint32_t sbase = lds_addr(smem);
+  f32x16_t dq[QH][JB];
+#pragma unroll
+  for (int qh = 0; qh < QH; ++qh)
+#pragma unroll
+    for (int j = 0; j < JB; ++j) dq[qh][j] = zero16();
+  const int nkb = (kend_blk + BKV - 1) / BKV;
+  const int wq = __builtin_amdgcn_readfirstlane(w);
+  const typename TK::template Dma<BKV, NTH> kd(H, wq);
+  const DsDma<NTH, NS> sd(qstride, wq);
+  auto issue = [&](int stage, int kb) {
+    uint16_t* st = smem + stage * STAGE;
+    const int rv = min(BKV, a.r - kb * BKV);
+    kd.issue(Kc + (long)kb * BKV * H, H, rv, st);
+    sd.issue(Sp + (long)kb * BKV * 32, qstride, rv, st + TILE_K);
+  };
+  for (int i = 0; i < ST - 1 && i < nkb; ++i) issue(i, i);
+  for (int kb = 0; kb < nkb; ++kb) {
+    if (kb + ST - 1 <= nkb) wait_vm<(ST - 2) * PER_ISSUE>();
+    else wait_vm<0>();
+    __builtin_amdgcn_s_barrier();
+    if (kb + ST - 1 < nkb) issue((kb + ST - 1) % ST, kb + ST - 1);
+    const uint32_t Kt = sbase + (kb % ST) * STAGE * 2, St = Kt + TILE_K * 2;
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) {
+      const int k0 = kb * BKV + 32 * sb;
+      // a 32-key block takes part when it starts before r and at or before the
+      // query block's last query: the blocks whose dS the dK kernel stored
+      bool act[QH], any = false;
+#pragma unroll
+      for (int qh = 0; qh < QH; ++qh) {
+        act[qh] = k0 < min(a.r, q_lo + 32 * (QH * w + qh) + 32);
+        any = any || act[qh];
+      }
+      if (!any) continue;
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        u32x4 kt[JB], db[QH];
+#pragma unroll
+        for (int j = 0; j < JB; ++j) kt[j] = TK::col8(Kt, 32 * sb + 16 * ks, 32 * j, lane);
+#pragma unroll
+        for (int qh = 0; qh < QH; ++qh) {
+          const int cb = 32 * (QH * w + qh);  // the block's 128-column sub-tile, column
+          db[qh] = col8_swapped(St + (cb >> 7) * BKV * 128 * 2, 32 * sb + 16 * ks, cb & 127, lane);
+        }
+        lgkm_wait(kt[0]);
+#pragma unroll
+        for (int j = 1; j < JB; ++j) lgkm_tie(kt[j]);
+#pragma unroll
+        for (int qh = 0; qh < QH; ++qh) lgkm_tie(db[qh]);
+        if (k0 + 32 > a.r) {
+#pragma unroll
+          for (int qh = 0; qh < QH; ++qh) db[qh] = mask_keys(db[qh], k0 + 16 * ks, G, a.r);
+        }
+#pragma unroll
+        for (int qh = 0; qh < QH; ++qh)
+          if (act[qh]) {
+#pragma unroll
+            for (int j = 0; j < JB; ++j) dq[qh][j] = mfma_t<F16>(kt[j], db[qh], dq[qh][j]);
+          }
+      }
+    }
+  }
+  // dq[qh][j][v]: column 32 j + 8 (v / 4) + 4 G + v % 4 of query
+  // q_lo + 32 (QH w + qh) + c
+#pragma unroll
+  for (int qh = 0; qh < QH; ++qh) {
+    const int t = q_lo + 32 * (QH * w + qh) + c;
+    if (t < a.r) {
+      uint16_t* dQ = (uint16_t*)a.dq + (long)(t - a.l) * a.ld_dq + h * D;
+#pragma unroll
+      for (int j = 0; j < JB; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; v += 4) {
+          const int col = 32 * j + 8 * (v >> 2) + 4 * G;
+          *(uint2*)(dQ + col) =
+              make_uint2(pack_bf16x2(dq[qh][j][v] * a.scale, dq[qh][j][v + 1] * a.scale),
+                         pack_bf16x2(dq[qh][j][v + 2] * a.scale, dq[qh][j][v + 3] * a.scale));
+        }
+    }
   }
 }
 
@@ -895,6 +1104,50 @@ hipError_t dq_d(const AttnArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Backward with stored dS, after the dV kernel: over query chunks of at most
+// cq rows (a multiple of 256) whose dS planes fit the scratch, the dK kernel
+// (MODE 3) writes the planes that the streaming dQ kernel then reads (the
+// rows' D = rowsum(dO * O) is already computed for the whole slice).
+template <int D, bool F16>
+hipError_t bwd_stored(const AttnArgs& a, hipStream_t s, long cq) {
+  constexpr int NWK = D == 128 ? 8 : 4, STK = D == 128 ? 4 : 2;
+  constexpr size_t lds_k = STK * (2 * 32 * D + NWK * 128) * 2 + 32 * NWK * D * 2;
+  // dQ: 256 queries per block (8 waves) when that fills the CUs, else 128
+  constexpr int STQ = 2;
+  constexpr size_t lds_q4 = STQ * (64 * D + 64 * 128) * 2, lds_q8 = STQ * (64 * D + 64 * 256) * 2;
+  const bool q8 = (long)cdiv(std::min<long>(a.r - a.l, cq), 256) * a.heads * a.bs >= 128;
+  hipError_t e = set_lds(attn_bwd_dkdv_mfma<D, NWK, 3, STK, F16>, lds_k);
+  if (e == hipSuccess)
+    e = q8 ? set_lds(attn_bwd_dq_stream<D, 8, 1, STQ, F16>, lds_q8)
+           : set_lds(attn_bwd_dq_stream<D, 4, 1, STQ, F16>, lds_q4);
+  if (e != hipSuccess) return e;
+  const int n = a.r - a.l;
+  for (int c0 = 0; c0 < n; c0 += (int)cq) {
+    const int c1 = (int)std::min<long>(n, c0 + cq);
+    AttnArgs b = a;
+    b.l = a.l + c0, b.r = a.l + c1;
+    b.q = (const uint16_t*)a.q + (long)c0 * a.ld;
+    b.o = (uint16_t*)a.o + (long)c0 * a.ld;
+    b.dout = (const uint16_t*)a.dout + (long)c0 * a.ld;
+    b.dq = (uint16_t*)a.dq + (long)c0 * a.ld_dq;
+    b.pd_ld = (long)cdiv(c1 - c0, 256) * 256;  // whole dQ blocks of either width
+    b.dst = a.pd;
+    attn_bwd_dkdv_mfma<D, NWK, 3, STK, F16>
+        <<<dim3(cdiv(b.r, 32 * NWK), a.heads, a.bs), 64 * NWK, lds_k, s>>>(b);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (q8)
+      attn_bwd_dq_stream<D, 8, 1, STQ, F16>
+          <<<dim3(cdiv(c1 - c0, 256), a.heads, a.bs), 512, lds_q8, s>>>(b);
+    else
+      attn_bwd_dq_stream<D, 4, 1, STQ, F16>
+          <<<dim3(cdiv(c1 - c0, 128), a.heads, a.bs), 256, lds_q4, s>>>(b);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 template <int D, bool F16>
 hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
   const int n = a.r - a.l;
@@ -935,6 +1188,11 @@ hipError_t bwd_d(const AttnArgs& a, hipStream_t s) {
       <<<dim3(cdiv(a.r, 32 * NWF), a.heads, a.bs), 64 * NWF, lds_a, s>>>(a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (a.pd) {
+    // query rows per chunk whose dS planes (whole 256-query blocks) fit
+    const long cq = a.pd_elems / ((long)a.bs * a.heads * a.r) / 256 * 256;
+    if (cq >= 256) return bwd_stored<D, F16>(a, s, cq);
+  }
   e = set_lds(attn_bwd_dkdv_mfma<D, NWK, 2, STK, F16>, lds_k);
   if (e != hipSuccess) return e;
   attn_bwd_dkdv_mfma<D, NWK, 2, STK, F16>

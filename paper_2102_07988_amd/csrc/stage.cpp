@@ -46,6 +46,8 @@ struct Scratch {
   size_t splitk_elems;
   float* attn;            // key-split partials of the query-parallel attention kernels
   size_t attn_elems;
+  uint16_t* pd;           // stored dS planes of the matrix-core attention backward
+  size_t pd_elems;
 };
 
 struct Carver {
@@ -200,6 +202,15 @@ size_t carve(const tp_stage_config* c, void* base, std::vector<LayerBufs>* lbs, 
     const size_t d = H / c->heads, qh = std::min<size_t>(L * a, 16384);
     s.attn_elems = 8 * (qh * d + 2 * qh);
     s.attn = (float*)cv.take(s.attn_elems * 4);
+  }
+  // the attention backward's stored dS (mixed path: matrix-core attention):
+  // 16-bit planes of every key for up to PD_ROWS query rows (whole 256-row
+  // blocks) of every head and sequence; longer slices run in query chunks
+  {
+    constexpr size_t PD_ROWS = 1024;
+    const size_t T = (size_t)c->max_seq;
+    s.pd_elems = mixed ? (size_t)batch_of(c) * a * T * std::min(PD_ROWS, (T + 255) / 256 * 256) : 0;
+    s.pd = (uint16_t*)cv.take(s.pd_elems * 2);
   }
   if (sc) *sc = s;
   return (cv.off + 255) & ~(size_t)255;
@@ -483,6 +494,7 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
     a.l = l, a.r = r, a.H = A, a.heads = S->heads, a.d = S->d, a.Lmax = S->L;
     a.bs = S->bsz, a.ld = S->bsz * A;
     a.ws = S->sc.attn, a.ws_elems = (long)S->sc.attn_elems;
+    a.pd = S->sc.pd, a.pd_elems = (long)S->sc.pd_elems;
     a.scale = 1.f / std::sqrt((float)S->d);
     a.q = rowp(B.q, lr, A, e), a.kc = B.kc, a.o = rowp(B.o, lr, A, e), a.lse = B.lse;
     a.vc = mx ? B.vb : B.vc;  // the backward's values are bf16

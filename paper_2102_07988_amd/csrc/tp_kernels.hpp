@@ -108,6 +108,15 @@ struct AttnArgs {
   // Host-side planning, as GemmArgs::need: the key-split partials' fp32
   // elements (forward: with the running maxima and sums), 0 without a split.
   long* need = nullptr;
+  // Backward scratch of pd_elems 16-bit elements for the stored dS planes
+  // (matrix-core path): the dK kernel writes dS and the dQ kernel streams it
+  // instead of recomputing the scores; slices whose planes do not fit run in
+  // query chunks.  Null: the recomputing dQ kernel.
+  uint16_t* pd = nullptr;
+  long pd_elems = 0;
+  // set by the launcher: the planes' base and their query columns
+  uint16_t* dst = nullptr;
+  long pd_ld = 0;
 };
 // The arguments of sequence blockIdx.z of the batch as a one-sequence view:
 // pointers moved to its columns (element type T) and planes; the row stride
