@@ -583,10 +583,12 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dkdv_mfma(AttnArgs a0) {
                                     smem + ST * STAGE);
     for (int i = 0; i < ST - 1 && i < nqb; ++i) issue(i, i);
   }
-  // MODE 3: a query block that takes part issues STORES store instructions,
-  // counted by vmcnt like the DMA; `recent` has bit j set when block qb - 1 - j
-  // did, so the stores of the ST - 1 blocks issued after tile qb's DMA may
-  // stay in flight while waiting for that tile
+  // MODE 3: a query block that takes part issues STORES store instructions
+  // (one 16-byte store per reduction half), counted by vmcnt like the DMA and
+  // completing in issue order with it; `recent` has bit j set when block
+  // qb - 1 - j did, so the stores of the ST - 1 blocks issued after tile qb's
+  // DMA may stay in flight while waiting for that tile.  Were more store
+  // instructions emitted, the wait would only be stricter.
   constexpr int STORES = 2;
   unsigned recent = 0;
   bool stored = false;
