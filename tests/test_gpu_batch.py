@@ -39,6 +39,14 @@ def test_matrix_core_batch_ragged(H, heads, wgrad):
           randomize_ln=True, label=f"mfma-attn d={H // heads} b=3")
 
 
+def test_batch_long_backward_slice_in_query_chunks():
+    """Two sequences and one 2048-token backward slice: the attention backward
+    runs it in two 1024-query chunks of stored dS planes (4 heads of d = 128),
+    after ragged forward slices; parity against one oracle run per sequence."""
+    _case(1, 512, 4, 2048, 2, "bf16", [1100, 948], [2048], "deferred", seeds=(31, 32, 33),
+          randomize_ln=True, label="b=2 query chunks")
+
+
 def test_fp32_batch_ragged():
     _case(2, 128, 4, 100, 2, "fp32", [37, 1, 29, 33], [50, 7, 43], "deferred", seeds=(3, 4, 5),
           randomize_ln=True, label="fp32 b=2")
