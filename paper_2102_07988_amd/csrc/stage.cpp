@@ -210,7 +210,7 @@ size_t carve(const tp_stage_config* c, void* base, std::vector<LayerBufs>* lbs, 
     constexpr size_t PD_ROWS = 1024;
     const size_t T = (size_t)c->max_seq;
     s.pd_elems = mixed ? (size_t)batch_of(c) * a * T * std::min(PD_ROWS, (T + 255) / 256 * 256) : 0;
-    s.pd = (uint16_t*)cv.take(s.pd_elems * 2);
+    s.pd = s.pd_elems ? (uint16_t*)cv.take(s.pd_elems * 2) : nullptr;
   }
   if (sc) *sc = s;
   return (cv.off + 255) & ~(size_t)255;

@@ -44,6 +44,16 @@ def test_head_widths(dtype):
         _case(1, H, heads, 48, dtype, [16, 32], label=f"d={H // heads}")
 
 
+@pytest.mark.parametrize("wgrad", ["per_slice", "deferred"])
+def test_stored_ds_backward_head_width_64(wgrad):
+    """32 heads of d = 64 on ragged slices: the backward slice ending at 640
+    has enough key blocks for the stored-dS path (the dK kernel writes dS, the
+    streaming kernel forms dQ = dS K), the one ending at 300 takes the
+    small-grid kernels."""
+    _case(1, 2048, 32, 640, "bf16", [200, 184, 256], [300, 340], wgrad, seeds=(41, 42, 43),
+          randomize_ln=True, label=f"d=64 stored dS {wgrad}")
+
+
 def test_gpt3_13b_shape_reduced_sequence():
     """hidden 5120, 40 heads (d = 128), bf16, two slices of 16 after nothing cached."""
     _case(1, 5120, 40, 32, "bf16", [16, 16], label="13B-shape")
