@@ -157,6 +157,9 @@ class Stage:
     def __init__(self, params: List[Dict[str, torch.Tensor]], hidden: int, heads: int,
                  max_seq: int, dtype: str = "bf16", wgrad: str = "per_slice",
                  ln_eps: float = 1e-5, device=None, batch: int = 1, op_parts: int = 1):
+        # the library handle, kept so the stage can be destroyed during interpreter
+        # shutdown, after the module's globals have been cleared
+        self._lib = lib
         self.n_layers = len(params)
         self.hidden, self.heads, self.max_seq, self.dtype = hidden, heads, max_seq, dtype
         self.batch = batch
@@ -193,7 +196,7 @@ class Stage:
     def __del__(self):
         h = getattr(self, "_h", None)
         if h is not None and h.value:
-            lib.tp_stage_destroy(h)
+            self._lib.tp_stage_destroy(h)
             self._h = None
 
     @property
