@@ -548,7 +548,17 @@ hipError_t ln_param_grads(int dtype, int n, int H, const void* du, const void* x
 __global__ void cvt_bf16_f16_kernel(size_t n, const uint16_t* src, uint16_t* dst, int vec) {
   const size_t stride = (size_t)gridDim.x * blockDim.x;
   if (vec) {
-    for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < n / 8; e += stride) {
+    const size_t n8 = n / 8;
+    size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    // four independent 16-byte loads in flight per thread
+    for (; e + 3 * stride < n8; e += 4 * stride) {
+      float v[4][8];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) ld8((const bf16*)src + 8 * (e + u * stride), v[u]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) st8((f16s*)dst + 8 * (e + u * stride), v[u]);
+    }
+    for (; e < n8; e += stride) {
       float v[8];
       ld8((const bf16*)src + 8 * e, v);
       st8((f16s*)dst + 8 * e, v);
