@@ -38,6 +38,16 @@ def test_matrix_core_shard_ragged(H, heads, p, wgrad):
           label=f"H={H} heads={heads} p={p}")
 
 
+@pytest.mark.parametrize("wgrad", ["per_slice", "deferred"])
+def test_shard_stored_ds_backward(wgrad):
+    """A 2-way shard with 16 local heads of d = 64 (attention width 1024 on a
+    2048 residual) over 1024 tokens: the backward slice ending at 1024 has
+    enough key blocks for the stored-dS path, the one ending at 400 takes the
+    small-grid kernels."""
+    _case(1, 2048, 32, 2, 1024, "bf16", [300, 100, 624], [400, 624], wgrad, seeds=(51, 52, 53),
+          label=f"shard p=2 stored dS {wgrad}")
+
+
 def test_shard_with_batch():
     """Operation partitioning and batch slices together (setting (10) of Table 1
     has both): two sequences through an 8-way shard."""
