@@ -229,14 +229,34 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_mfma_kernel(GemmArgs a) {
       }
 }
 
+// The partial planes that hold column n: their first element for row 0 and
+// column n, the row stride and plane size, and their count (two column groups,
+// see GemmArgs::split_cols, or one).
+struct SplitPlanes {
+  const float* p;
+  long ld, plane;
+  int count;
+};
+__device__ inline SplitPlanes split_planes(const GemmArgs& a, int n) {
+  if (a.split_cols && n >= a.split_cols) {
+    const long ld = a.N - a.split_cols;
+    return {a.ws + (long)a.splits * a.M * a.split_cols + (n - a.split_cols), ld, a.M * ld,
+            a.splits2};
+  }
+  const long ld = a.split_cols ? a.split_cols : a.N;
+  return {a.ws + n, ld, a.M * ld, a.splits};
+}
+
 // Sums the split partials in split order (deterministic) and applies the epilogue.
 template <int EPI>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
   const long tot = (long)a.M * a.N;
   for (long e = (long)blockIdx.x * 256 + threadIdx.x; e < tot; e += (long)gridDim.x * 256) {
+    const int m = (int)(e / a.N), n = (int)(e % a.N);
+    const SplitPlanes sp = split_planes(a, n);
     float s = 0.f;
-    for (int z = 0; z < a.splits; ++z) s += a.ws[(long)z * tot + e];
-    epi1<bf16, EPI>(a, (int)(e / a.N), (int)(e % a.N), s);
+    for (int z = 0; z < sp.count; ++z) s += sp.p[z * sp.plane + m * sp.ld];
+    epi1<bf16, EPI>(a, m, n, s);
   }
 }
 
@@ -246,13 +266,15 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
 // pointer 16-byte aligned (checked by the launcher).
 template <int EPI>
 __global__ __launch_bounds__(256) void splitk_reduce8_kernel(GemmArgs a) {
-  const long tot8 = (long)a.M * a.N / 8, plane = (long)a.M * a.N;
+  const long tot8 = (long)a.M * a.N / 8;
   const int n8 = a.N / 8;
   for (long e = (long)blockIdx.x * 256 + threadIdx.x; e < tot8; e += (long)gridDim.x * 256) {
     const int m = (int)(e / n8), n = (int)(e % n8) * 8;
+    // split_cols is a multiple of 8: the 8 columns lie in one group
+    const SplitPlanes sp = split_planes(a, n);
     float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int z = 0; z < a.splits; ++z) {
-      const float4* p = (const float4*)(a.ws + z * plane + (long)m * a.N + n);
+    for (int z = 0; z < sp.count; ++z) {
+      const float4* p = (const float4*)(sp.p + z * sp.plane + (long)m * sp.ld);
       const float4 u = p[0], w = p[1];
       s[0] += u.x, s[1] += u.y, s[2] += u.z, s[3] += u.w;
       s[4] += w.x, s[5] += w.y, s[6] += w.z, s[7] += w.w;

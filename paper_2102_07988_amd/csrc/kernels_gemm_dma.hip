@@ -561,14 +561,44 @@ hipError_t launch_dma(const GemmArgs& a, hipStream_t s) {
 // reduction is split (whole k-tiles, the last split may be shorter).
 // force_splits > 0 takes that many splits (at most; as k-tiles allow),
 // otherwise the split count comes from the cost model below (<= 8 splits of
-// >= 8 k-tiles).
+// >= 8 k-tiles).  With splits2 > 0 and 0 < cols1 < the column-tile count, the
+// product runs as two split launches: column tiles [0, cols1) with
+// force_splits splits, the rest with splits2 (when the partials fit), and one
+// reduction over both.
 template <int BM, int BN, int BK, int WGM, int WGN, bool A_KC, bool B_KC, int STAGES,
           int SB, bool F16>
-hipError_t run_dma(GemmArgs a, hipStream_t s, int force_splits = 0) {
+hipError_t run_dma(GemmArgs a, hipStream_t s, int force_splits = 0, int splits2 = 0,
+                   int cols1 = 0) {
   constexpr int CUS = 256;
   if (a.K % BK) return hipErrorNotSupported;
   const long tiles = (long)cdiv(a.M, BM) * cdiv(a.N, BN);
   const int nkt = a.K / BK;
+  if (force_splits > 0 && splits2 > 0 && cols1 > 0 && (long)cols1 * BN < a.N && a.ws) {
+    const int n1 = cols1 * BN, n2 = a.N - n1;
+    const int ks1 = cdiv(nkt, std::min(force_splits, nkt)) * BK;
+    const int ks2 = cdiv(nkt, std::min(splits2, nkt)) * BK;
+    const int s1 = cdiv(a.K, ks1), s2 = cdiv(a.K, ks2);
+    const long p1 = (long)s1 * a.M * n1, need = p1 + (long)s2 * a.M * n2;
+    if (need <= a.ws_elems) {
+      if (a.need) {
+        *a.need = need;
+        return hipSuccess;
+      }
+      GemmArgs g = a;
+      g.N = n1, g.k_split = ks1, g.splits = s1;
+      hipError_t e = launch_dma<BM, BN, BK, WGM, WGN, A_KC, B_KC, STAGES, SB, true, F16>(g, s);
+      if (e != hipSuccess) return e;
+      g = a;
+      g.N = n2, g.k_split = ks2, g.splits = s2;
+      g.B = (const uint16_t*)a.B + (long)n1 * a.sbn;
+      g.ws = a.ws + p1, g.ws_elems = a.ws_elems - p1;
+      e = launch_dma<BM, BN, BK, WGM, WGN, A_KC, B_KC, STAGES, SB, true, F16>(g, s);
+      if (e != hipSuccess) return e;
+      GemmArgs r = a;
+      r.splits = s1, r.splits2 = s2, r.split_cols = n1;
+      return gemm_splitk_reduce(r, s);
+    }
+  }
   int splits = 1;
   if (force_splits > 0) {
     splits = a.ws && (long)force_splits * a.M * a.N <= a.ws_elems ? std::min(force_splits, nkt) : 1;
@@ -605,15 +635,18 @@ hipError_t run_dma(GemmArgs a, hipStream_t s, int force_splits = 0) {
 }
 
 template <bool A_KC, bool B_KC, bool F16 = false>
-hipError_t run_cfg_id(int cfg, const GemmArgs& a, hipStream_t s, int splits = 0) {
+hipError_t run_cfg_id(int cfg, const GemmArgs& a, hipStream_t s, int splits = 0, int splits2 = 0,
+                      int cols1 = 0) {
   switch (cfg) {
     case 0: return run_dma<128, 128, 64, 2, 2, A_KC, B_KC, 4, 4, F16>(a, s, splits);
     case 1: return run_dma<256, 128, 64, 4, 2, A_KC, B_KC, 3, 3, F16>(a, s, splits);
     case 2: return run_dma<256, 256, 64, 2, 4, A_KC, B_KC, 2, 2, F16>(a, s, splits);
-    case 3: return run_dma<256, 256, 64, 2, 4, A_KC, B_KC, 2, 3, F16>(a, s, splits);
+    case 3:
+      return run_dma<256, 256, 64, 2, 4, A_KC, B_KC, 2, 3, F16>(a, s, splits, splits2, cols1);
     case 4:
       // 256 x 192: 256 tiles for a 256-row product of width 49152, 64 for 12288
-      if constexpr (A_KC) return run_dma<256, 192, 64, 4, 2, A_KC, B_KC, 2, 3, F16>(a, s, splits);
+      if constexpr (A_KC)
+        return run_dma<256, 192, 64, 4, 2, A_KC, B_KC, 2, 3, F16>(a, s, splits, splits2, cols1);
       else return hipErrorNotSupported;
     default: return hipErrorNotSupported;
   }
@@ -632,6 +665,7 @@ hipError_t run_cfg_id(int cfg, const GemmArgs& a, hipStream_t s, int splits = 0)
 // workgroups, not below the weight stream from HBM, plus the partial sums.
 struct TileChoice {
   int cfg, splits;
+  int splits2 = 0, cols1 = 0;  // two column groups (see run_dma), 0: one launch
 };
 TileChoice choose_tiles(const GemmArgs& a) {
   static const int kSplits[] = {1, 2, 3, 4, 5, 6, 8, 10, 12, 16};
@@ -660,6 +694,42 @@ TileChoice choose_tiles(const GemmArgs& a) {
       }
     }
   }
+  // Two launches over column groups: the first group's workgroups fill whole
+  // rounds, the second group takes its own split count, so no round runs
+  // part-empty the way a uniform split leaves the last one (the query/key/value
+  // product of 144 tiles of 256 x 256: 2 x 128 + 16 x 16 workgroups against 3
+  // x 144).  Taken when the model puts it 3 % under the best single launch.
+  const double single = best;
+  for (const Cand& c : kCands) {
+    if (c.bm != 256 || c.bn < 192) continue;
+    const long mt = cdiv(a.M, c.bm), tn = cdiv(a.N, c.bn);
+    for (int sp1 : kSplits) {
+      if (sp1 > nkt) break;
+      const int ks1 = cdiv(nkt, sp1), e1 = cdiv(nkt, ks1);
+      for (long r1 = 1;; ++r1) {
+        const long cols1 = r1 * 256 / (mt * e1);
+        if (cols1 >= tn) break;
+        if (cols1 * mt * e1 != r1 * 256) continue;
+        const long n1 = cols1 * c.bn, n2 = a.N - n1;
+        const double hbm1 = (double)mt * n1 * a.K * 2.0 / 1e6 * 0.1773;
+        const double hbm2 = (double)mt * n2 * a.K * 2.0 / 1e6 * 0.1773;
+        for (int sp2 : kSplits) {
+          if (sp2 > nkt) break;
+          const int ks2 = cdiv(nkt, sp2), e2 = cdiv(nkt, ks2);
+          const double part = (double)e1 * a.M * n1 + (double)e2 * a.M * n2;
+          if (!a.ws || part > (double)a.ws_elems) break;
+          const long r2 = cdiv(mt * (tn - cols1) * e2, 256);
+          double t = std::max(r1 * (0.7377 + ks1 * c.c_kt), hbm1) +
+                     std::max(r2 * (0.7377 + ks2 * c.c_kt), hbm2);
+          t += 5.6764 + part * 8.0 / 1e6 / 5.7874;
+          if (t < best && t < 0.97 * single) {
+            best = t;
+            pick = {c.cfg, e1, e2, (int)cols1};
+          }
+        }
+      }
+    }
+  }
   return pick;
 }
 
@@ -682,7 +752,7 @@ hipError_t gemm_dma_bf16_cfg(int cfg, const GemmArgs& a, hipStream_t s) {
   // operands) as 8-column segments
   if (a.epi == EPI_ACC_F32 && (((uintptr_t)a.C & 15) || (a.ldc & 3))) return hipErrorNotSupported;
   if (a.epi != EPI_ACC_F32 && !vec8_ok(a)) return hipErrorNotSupported;
-  int splits = 0;
+  int splits = 0, splits2 = 0, cols1 = 0;
   if (cfg < 0) {
     // weight-gradient products (both operands m/n-contiguous): 256 x 256 tiles
     // over one (A, B) ring; products with a weight matrix as B: the modelled
@@ -694,16 +764,18 @@ hipError_t gemm_dma_bf16_cfg(int cfg, const GemmArgs& a, hipStream_t s) {
       const TileChoice c = choose_tiles(a);
       cfg = c.cfg;
       splits = c.splits;
+      splits2 = c.splits2;
+      cols1 = c.cols1;
     }
   }
   if (a.in_f16) {
     // fp16 operands: the query/key/value product (activations times the fp16
     // weight copy, both k-contiguous)
     if (!(a_kc && b_kc) || a.epi != EPI_QKV) return hipErrorNotSupported;
-    return run_cfg_id<true, true, true>(cfg, a, s, splits);
+    return run_cfg_id<true, true, true>(cfg, a, s, splits, splits2, cols1);
   }
-  if (a_kc && b_kc) return run_cfg_id<true, true>(cfg, a, s, splits);
-  if (a_kc && b_nc) return run_cfg_id<true, false>(cfg, a, s, splits);
+  if (a_kc && b_kc) return run_cfg_id<true, true>(cfg, a, s, splits, splits2, cols1);
+  if (a_kc && b_nc) return run_cfg_id<true, false>(cfg, a, s, splits, splits2, cols1);
   if (a_mc && b_nc) {
     if (a.M < 128 || a.N < 128) return hipErrorNotSupported;
     return run_cfg_id<false, false>(cfg, a, s);

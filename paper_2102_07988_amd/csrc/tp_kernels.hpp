@@ -51,6 +51,11 @@ struct GemmArgs {
   long ws_elems = 0;
   // set by the launcher: reduction range of one split and the split count
   int k_split = 0, splits = 1;
+  // set by the launcher for a split product run as two launches over column
+  // groups: columns [0, split_cols) leave `splits` partial planes of split_cols
+  // columns, columns [split_cols, N) `splits2` planes of N - split_cols
+  // columns after them; 0 for one launch over every column
+  int split_cols = 0, splits2 = 0;
   // set by the launcher: output-tile order (0 grid order, 1 XCD super-tiles)
   int walk = 0;
   // Host-side planning: when set, the launcher launches nothing and stores
