@@ -22,6 +22,8 @@ more), unsplit d = 128 dQ launches.
   gradients with 4 x 512 backward slices.
 * One GPU's shard of the paper's 175B settings with operation partitioning
   (Table 1 settings (10) and (9)): 8-way (2 layers) and 4-way (1 layer).
+* Hidden 11136 (87 heads), whose query/key/value product runs as two split
+  launches over column groups, the second ending in a partial tile.
 * The largest shapes the stage accepts: hidden 16384 (128 heads, one layer,
   256 tokens in ragged slices), and the longest sequence, 20344 tokens (the
   generic attention's one-row-per-block LDS limit; hidden 256, 2 heads of
@@ -175,6 +177,18 @@ def test_maximum_hidden_size():
               "hidden 16384, per-slice dW")
     check_run(ref, params, x, dy, H, heads, L, "bf16", [100, 156], None, "deferred",
               "hidden 16384, deferred dW")
+
+
+def test_two_group_split_with_ragged_tail():
+    """Hidden 11136 (87 heads of 128), one layer, 256 tokens: the tile model runs
+    the 33408-wide query/key/value product as two split launches over column
+    groups (128 tiles of 256 columns, then the last 2.5 tiles), the second
+    ending in a partial tile."""
+    H, heads, L = 11136, 87, 256
+    params, x, dy = inputs(1, H, L, "bf16")
+    ref = oracle(params, x, dy, heads)
+    check_run(ref, params, x, dy, H, heads, L, "bf16", [256], None, "deferred",
+              "hidden 11136, two-group query/key/value product")
 
 
 def test_maximum_sequence_length():
