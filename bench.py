@@ -46,19 +46,20 @@ PEAK_HBM_GBS = 8000.0
 # HBM bytes per launch of a kernel class on the default workload, from two
 # rocprofv3 --pmc passes (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on
 # a plain copy of known size (profiles/gemm_bwd_dw_tn_traffic.md).  Reported only
-# while the kernel source still has the hash it had when the counters were taken.
+# while the kernel source still has the hash it had when the counters were taken,
+# and for the gradient-buffer mode they were taken in.
 TRAFFIC = {
-    "gemm_bwd_dw_tn": {"workload": "gpt3-175b-stage",
+    "gemm_bwd_dw_tn": {"workload": "gpt3-175b-stage", "grad_buffers": "overwrite",
                        "source": "paper_2102_07988_amd/csrc/kernels_gemm_dma.hip",
-                       "sha256_16": "0c9119a7a0d01de0", "bytes_per_launch": 6603684408},
+                       "sha256_16": "a97547c36515da7b", "bytes_per_launch": 4549985731},
 }
 
 
-def measured_traffic(kernel: str, workload: str):
+def measured_traffic(kernel: str, workload: str, grad_buffers: str):
     import hashlib
 
     t = TRAFFIC.get(kernel)
-    if not t or t["workload"] != workload:
+    if not t or t["workload"] != workload or t["grad_buffers"] != grad_buffers:
         return None
     try:
         h = hashlib.sha256(open(os.path.join(ROOT, t["source"]), "rb").read()).hexdigest()[:16]
@@ -330,6 +331,10 @@ def main():
                     help="'uniform256', comma-separated lengths, or 'dp' (DP over this stage's "
                          "model-mode cost table at the paper's K for the model)")
     ap.add_argument("--wgrad", default="deferred", choices=["deferred", "per_slice"])
+    ap.add_argument("--accumulate-grads", action="store_true",
+                    help="each step adds its parameter gradients to the earlier steps' "
+                         "(default: each step is a training iteration of one sequence that "
+                         "stores its gradients, TP_SEQ_OVERWRITE_GRADS)")
     ap.add_argument("--cpu-baseline-tokens", type=int, default=96)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
@@ -412,7 +417,7 @@ def main():
         bounds.append(bounds[-1] + n)
 
     def step():
-        st.reset()
+        st.reset(overwrite_grads=not args.accumulate_grads)
         for i in range(len(lens)):
             l, r = bounds[i], bounds[i + 1]
             st.forward(l, r, x[l:r], out=y[l:r])
@@ -485,7 +490,8 @@ def main():
             dom = "gemm_bwd_dw_tn"
         s = stats[dom]
         secs = s["total_ms"] * 1e-3
-        traffic = measured_traffic(dom, args.workload)
+        traffic = measured_traffic(dom, args.workload,
+                                   "accumulate" if args.accumulate_grads else "overwrite")
         if dom.startswith("gemm"):
             ach = s["flops"] / secs / 1e12
             roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2),
@@ -505,6 +511,7 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": args.workload, "layers": n_layers, "hidden": H, "heads": heads,
                    "seq_len": L, "batch": 1, "slicing": lens, "wgrad": args.wgrad,
+                   "grad_buffers": "accumulate" if args.accumulate_grads else "overwrite",
                    **({"slicing_source": dp_source} if dp_source else {}),
                    "global_batch": 1,
                    "parallelism": "one pipeline stage" if parts == 1 else
@@ -523,7 +530,7 @@ def main():
                 b.append(b[-1] + n)
 
             def seq():
-                st.reset()
+                st.reset(overwrite_grads=not args.accumulate_grads)
                 for i in range(len(sl)):
                     st.forward(b[i], b[i + 1], x[b[i]:b[i + 1]], out=y[b[i]:b[i + 1]])
                 for i in range(len(sl) - 1, -1, -1):

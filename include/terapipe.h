@@ -26,7 +26,9 @@
  *    that is current when tp_stage_init is called; the stage keeps pointers
  *    only.  Matrices are row-major; weight matrices are [out][in].
  *  - Activations and parameters use the stage dtype (bf16 or fp32); gradients
- *    are always fp32 and are ACCUMULATED (+=): the caller zeroes them.
+ *    are always fp32 and are ACCUMULATED (+=): the caller zeroes them, or
+ *    starts the sequence with tp_kv_prefix_reset_ex(TP_SEQ_OVERWRITE_GRADS)
+ *    to have its gradients stored in place of the old contents.
  *  - Precision of a bf16 stage whose head width is 64 or 128: matrix products
  *    take bf16 operands with fp32 accumulation, except that (1) the residual
  *    stream inside the stage (the input of every layer but the first, and x1)
@@ -144,6 +146,27 @@ void tp_stage_destroy(tp_stage *stage);
  * start out empty (Sec. 3.2: the cell keeps them from slice to slice).
  * Parameter gradients are not touched. */
 tp_status tp_kv_prefix_reset(tp_stage *stage);
+
+/* Flags of tp_kv_prefix_reset_ex. */
+#define TP_SEQ_OVERWRITE_GRADS 1u
+
+/* tp_kv_prefix_reset, plus per-sequence flags (0 = tp_kv_prefix_reset).
+ * TP_SEQ_OVERWRITE_GRADS: the sequence's first write of each parameter
+ * gradient stores its value instead of adding it, so the gradients end up as
+ * this sequence's alone, exactly as if the caller had zeroed them first (a
+ * training iteration's first sequence; later sequences of the same iteration
+ * start with flags 0 and add).  The gradient buffers' earlier contents are
+ * never read and may be anything, NaN included.  The first write is the
+ * first backward slice with TP_WGRAD_PER_SLICE, the backward slice that
+ * reaches position 0 with TP_WGRAD_DEFERRED (the only one that writes
+ * gradients); a DEFERRED sequence whose backward never reaches 0 writes none.
+ * This changes no value the method computes (Sec. 4: TeraPipe trains with
+ * the same gradients as whole-sequence processing); it saves the read of
+ * every fp32 gradient in the weight-gradient GEMMs' epilogues and the
+ * caller's zeroing pass.
+ * Errors: TP_ERR_INVALID (null stage, unknown flag bits; nothing enqueued),
+ * TP_ERR_HIP. */
+tp_status tp_kv_prefix_reset_ex(tp_stage *stage, unsigned flags);
 
 /* Forward of token slice [l, r) through every layer (Sec. 3.2).
  * x: [r-l][b][H] stage input rows, y: [r-l][b][H] stage output rows (stage

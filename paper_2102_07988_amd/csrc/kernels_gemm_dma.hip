@@ -424,10 +424,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
              ec;
     };
     // fp32 +=: the destination values of the next P sub-tiles are in flight
-    // while one is combined
+    // while one is combined (a plain store with a.overwrite)
     constexpr int T = FM * FN, P = T < 4 ? T : 4;
+    const bool add = !SPLIT && !a.overwrite;
     float4 pre[P][4];
-    if (!SPLIT && full) {
+    if (add && full) {
 #pragma unroll
       for (int t = 0; t < P; ++t)
 #pragma unroll
@@ -445,13 +446,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
       if (full) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          if constexpr (!SPLIT) {
+          if (add) {
             const float4 o = pre[t % P][q];
             x[q].x += o.x, x[q].y += o.y, x[q].z += o.z, x[q].w += o.w;
           }
           *(float4*)dst_of(t, q) = x[q];
         }
-        if (!SPLIT && t + P < T) {
+        if (add && t + P < T) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) pre[t % P][q] = *(const float4*)dst_of(t + P, q);
         }
@@ -465,7 +466,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
             const float xs[4] = {x[q].x, x[q].y, x[q].z, x[q].w};
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-              if (n + e < a.N) dst[e] = SPLIT ? xs[e] : dst[e] + xs[e];
+              if (n + e < a.N) dst[e] = add ? dst[e] + xs[e] : xs[e];
           }
         }
       }

@@ -387,7 +387,7 @@ template <typename T, typename TX>
 __global__ __launch_bounds__(256) void ln_param_grads_kernel(int n, int H, const T* du,
                                                              const TX* x, const float* mean,
                                                              const float* rstd, float* dg,
-                                                             float* db) {
+                                                             float* db, int store) {
   __shared__ float pg[CR_RG][CR_COLS + 1], pb[CR_RG][CR_COLS + 1], q[2][8 * (CR_COLS + 1)];
   const int cc = threadIdx.x & 3, rg = threadIdx.x >> 2;
   const int c0 = blockIdx.x * CR_COLS + cc * 8;
@@ -424,14 +424,14 @@ __global__ __launch_bounds__(256) void ln_param_grads_kernel(int n, int H, const
   const float b = col_partials_sum(pb, q[1]);
   const int col = blockIdx.x * CR_COLS + threadIdx.x;
   if (threadIdx.x < CR_COLS && col < H) {
-    dg[col] += a;
-    db[col] += b;
+    dg[col] = store ? a : dg[col] + a;
+    db[col] = store ? b : db[col] + b;
   }
 }
 
 template <typename T>
 __global__ __launch_bounds__(256) void colsum_kernel(int n, int N, const T* A, long lda,
-                                                     float* out) {
+                                                     float* out, int store) {
   __shared__ float ps[CR_RG][CR_COLS + 1], q[8 * (CR_COLS + 1)];
   const int cc = threadIdx.x & 3, rg = threadIdx.x >> 2;
   const int c0 = blockIdx.x * CR_COLS + cc * 8;
@@ -454,7 +454,7 @@ __global__ __launch_bounds__(256) void colsum_kernel(int n, int N, const T* A, l
   __syncthreads();
   const float a = col_partials_sum(ps, q);
   const int col = blockIdx.x * CR_COLS + threadIdx.x;
-  if (threadIdx.x < CR_COLS && col < N) out[col] += a;
+  if (threadIdx.x < CR_COLS && col < N) out[col] = store ? a : out[col] + a;
 }
 
 // dK and dV (fp32, [n, H]) into the K and V thirds of the dQKV rows, 8
@@ -527,20 +527,20 @@ hipError_t ln_bwd(int dtype, int n, int H, const void* du, const void* x, int x_
 }
 
 hipError_t ln_param_grads(int dtype, int n, int H, const void* du, const void* x, int x_f32,
-                          const float* mean, const float* rstd, float* dg, float* db,
+                          const float* mean, const float* rstd, float* dg, float* db, int store,
                           hipStream_t s) {
   clear_stale_error();
   if (n <= 0) return hipSuccess;
   const int blocks = cdiv(H, CR_COLS);
   if (dtype == DT_FP32)
     ln_param_grads_kernel<float, float><<<blocks, 256, 0, s>>>(n, H, (const float*)du,
-                                                               (const float*)x, mean, rstd, dg, db);
+                                                               (const float*)x, mean, rstd, dg, db, store);
   else if (x_f32)
     ln_param_grads_kernel<bf16, float><<<blocks, 256, 0, s>>>(n, H, (const bf16*)du,
-                                                              (const float*)x, mean, rstd, dg, db);
+                                                              (const float*)x, mean, rstd, dg, db, store);
   else
     ln_param_grads_kernel<bf16, bf16><<<blocks, 256, 0, s>>>(n, H, (const bf16*)du,
-                                                             (const bf16*)x, mean, rstd, dg, db);
+                                                             (const bf16*)x, mean, rstd, dg, db, store);
   return hipGetLastError();
 }
 
@@ -579,15 +579,15 @@ hipError_t cvt_bf16_f16(size_t n, const void* src, void* dst, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t colsum_acc(int dtype, int n, int N, const void* A, long lda, float* out,
+hipError_t colsum_acc(int dtype, int n, int N, const void* A, long lda, float* out, int store,
                       hipStream_t s) {
   clear_stale_error();
   if (n <= 0 || N <= 0) return hipSuccess;
   const int blocks = cdiv(N, CR_COLS);
   if (dtype == DT_FP32)
-    colsum_kernel<float><<<blocks, 256, 0, s>>>(n, N, (const float*)A, lda, out);
+    colsum_kernel<float><<<blocks, 256, 0, s>>>(n, N, (const float*)A, lda, out, store);
   else
-    colsum_kernel<bf16><<<blocks, 256, 0, s>>>(n, N, (const bf16*)A, lda, out);
+    colsum_kernel<bf16><<<blocks, 256, 0, s>>>(n, N, (const bf16*)A, lda, out, store);
   return hipGetLastError();
 }
 

@@ -91,6 +91,9 @@ struct tp_stage {
   // a sequence has been started by tp_kv_prefix_reset since the stage was
   // created or last profiled (the dK/dV buffer is zero, the fp16 W_qkv copy taken)
   bool prepared = false;
+  // the sequence's next gradient writes store rather than add
+  // (TP_SEQ_OVERWRITE_GRADS; cleared once every gradient has been written)
+  bool grad_store = false;
   bool profiling = false;
   // planning pass (tp_slice_forward_static): no launch, only the largest
   // partial-sum scratch (fp32 elements) the slice's kernels would take
@@ -266,7 +269,7 @@ hipError_t launch(tp_stage* S, int cls, double flops, double bytes, Fn&& fn) {
 double gemm_bytes(const GemmArgs& g, size_t esz) {
   double b = ((double)g.M * g.K + (double)g.K * g.N) * esz;
   if (g.epi == EPI_ACC_F32)
-    b += 8.0 * g.M * g.N;
+    b += (g.overwrite ? 4.0 : 8.0) * g.M * g.N;
   else
     b += (double)g.M * g.N * esz * (g.epi == EPI_GELU ? 2 : 1) +
          (g.epi == EPI_RESID || g.epi == EPI_DGELU ? (double)g.M * g.N * esz : 0.0);
@@ -320,14 +323,16 @@ tp_status wgrad_gemms(tp_stage* S, int li, int l, int n) {
   const size_t e = S->esz;
   LayerBufs& B = S->lb[li];
   tp_layer_ptrs& G = S->G[li];
-  TRY(run_gemm(S, K_GEMM_DW, tn(H, F, n, rowp(B.dy, l, H, e), H, rowp(B.g, l, F, e), F,
-                                (float*)G.w_fc2)));
-  TRY(run_gemm(S, K_GEMM_DW, tn(F, H, n, rowp(B.dz, l, F, e), F, rowp(B.u2, l, H, e), H,
-                                (float*)G.w_fc1)));
-  TRY(run_gemm(S, K_GEMM_DW, tn(H, A, n, rowp(B.dx1, l, H, e), H, rowp(B.o, l, A, e), A,
-                                (float*)G.w_o)));
-  TRY(run_gemm(S, K_GEMM_DW, tn(3 * A, H, n, rowp(B.dqkv, l, 3 * A, e), 3 * A,
-                                rowp(B.u, l, H, e), H, (float*)G.w_qkv)));
+  const int ow = S->grad_store;
+  GemmArgs g[4] = {
+      tn(H, F, n, rowp(B.dy, l, H, e), H, rowp(B.g, l, F, e), F, (float*)G.w_fc2),
+      tn(F, H, n, rowp(B.dz, l, F, e), F, rowp(B.u2, l, H, e), H, (float*)G.w_fc1),
+      tn(H, A, n, rowp(B.dx1, l, H, e), H, rowp(B.o, l, A, e), A, (float*)G.w_o),
+      tn(3 * A, H, n, rowp(B.dqkv, l, 3 * A, e), 3 * A, rowp(B.u, l, H, e), H, (float*)G.w_qkv)};
+  for (GemmArgs& gi : g) {
+    gi.overwrite = ow;
+    TRY(run_gemm(S, K_GEMM_DW, gi));
+  }
   return TP_OK;
 }
 
@@ -340,19 +345,22 @@ tp_status deferred_param_reductions(tp_stage* S, int li, int rows) {
   hipStream_t st = S->stream;
   LayerBufs& B = S->lb[li];
   tp_layer_ptrs& G = S->G[li];
-  TRY(launch(S, K_MISC, 0, nb, [&] { return colsum_acc(dt, rows, H, B.dy, H, (float*)G.b_fc2, st); }));
+  const int ow = S->grad_store;
+  TRY(launch(S, K_MISC, 0, nb,
+             [&] { return colsum_acc(dt, rows, H, B.dy, H, (float*)G.b_fc2, ow, st); }));
   TRY(launch(S, K_MISC, 0, (double)rows * F * e,
-             [&] { return colsum_acc(dt, rows, F, B.dz, F, (float*)G.b_fc1, st); }));
+             [&] { return colsum_acc(dt, rows, F, B.dz, F, (float*)G.b_fc1, ow, st); }));
   TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
     return ln_param_grads(dt, rows, H, B.du2, B.x1, S->mixed, B.mean2, B.rstd2, (float*)G.ln2_g,
-                          (float*)G.ln2_b, st);
+                          (float*)G.ln2_b, ow, st);
   }));
-  TRY(launch(S, K_MISC, 0, nb, [&] { return colsum_acc(dt, rows, H, B.dx1, H, (float*)G.b_o, st); }));
+  TRY(launch(S, K_MISC, 0, nb,
+             [&] { return colsum_acc(dt, rows, H, B.dx1, H, (float*)G.b_o, ow, st); }));
   TRY(launch(S, K_MISC, 0, 3.0 * rows * A * e,
-             [&] { return colsum_acc(dt, rows, 3 * A, B.dqkv, 3 * A, (float*)G.b_qkv, st); }));
+             [&] { return colsum_acc(dt, rows, 3 * A, B.dqkv, 3 * A, (float*)G.b_qkv, ow, st); }));
   TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
     return ln_param_grads(dt, rows, H, B.du, B.x_in, S->mixed, B.mean1, B.rstd1, (float*)G.ln1_g,
-                          (float*)G.ln1_b, st);
+                          (float*)G.ln1_b, ow, st);
   }));
   return TP_OK;
 }
@@ -444,6 +452,7 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
   const bool per_slice = S->cfg.wgrad_mode == TP_WGRAD_PER_SLICE;
   const double nb = (double)n * H * e;
   const bool mx = S->mixed;
+  const int ow = S->grad_store;
   for (int li = NL - 1; li >= 0; --li) {
     LayerBufs& B = S->lb[li];
     const tp_layer_ptrs& P = S->P[li];
@@ -458,7 +467,7 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
     g.epi = EPI_DGELU, g.R = rowp(B.z, lr, F, e), g.ldr = F, g.C = rowp(B.dz, lr, F, e), g.ldc = F;
     TRY(run_gemm(S, K_GEMM_DX, g));
     if (per_slice)
-      TRY(launch(S, K_MISC, 0, nb, [&] { return colsum_acc(dt, n, H, dyl, H, (float*)G.b_fc2, st); }));
+      TRY(launch(S, K_MISC, 0, nb, [&] { return colsum_acc(dt, n, H, dyl, H, (float*)G.b_fc2, ow, st); }));
     // LayerNorm output gradients: per-slice scratch, or (deferred mode) rows of
     // per-layer arenas kept for the once-per-sequence parameter reductions
     void* du2 = per_slice ? S->sc.du2 : rowp(B.du2, lr, H, e);
@@ -469,7 +478,7 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
     TRY(run_gemm(S, K_GEMM_DX, g));
     if (per_slice)
       TRY(launch(S, K_MISC, 0, (double)n * F * e, [&] {
-        return colsum_acc(dt, n, F, rowp(B.dz, lr, F, e), F, (float*)G.b_fc1, st);
+        return colsum_acc(dt, n, F, rowp(B.dz, lr, F, e), F, (float*)G.b_fc1, ow, st);
       }));
     // LN2 backward + residual: dx1 = dy + LN2^T(du2)
     TRY(launch(S, K_NORM, 0, 4 * nb, [&] {
@@ -479,7 +488,7 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
     if (per_slice)
       TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
         return ln_param_grads(dt, n, H, du2, x1, mx, B.mean2 + lr, B.rstd2 + lr,
-                              (float*)G.ln2_g, (float*)G.ln2_b, st);
+                              (float*)G.ln2_g, (float*)G.ln2_b, ow, st);
       }));
     // output projection backward: dO = dx1 W_o
     g = nn(n, A, H, rowp(B.dx1, lr, H, e), H, P.w_o);
@@ -487,7 +496,7 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
     TRY(run_gemm(S, K_GEMM_DX, g));
     if (per_slice)
       TRY(launch(S, K_MISC, 0, nb, [&] {
-        return colsum_acc(dt, n, H, rowp(B.dx1, lr, H, e), H, (float*)G.b_o, st);
+        return colsum_acc(dt, n, H, rowp(B.dx1, lr, H, e), H, (float*)G.b_o, ow, st);
       }));
     // attention backward: dq rows, dK/dV into the fp32 buffer for keys [0, r)
     AttnArgs a;
@@ -516,7 +525,7 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
     TRY(run_gemm(S, K_GEMM_DX, g));
     if (per_slice)
       TRY(launch(S, K_MISC, 0, 3.0 * n * A * e, [&] {
-        return colsum_acc(dt, n, 3 * A, rowp(B.dqkv, lr, 3 * A, e), 3 * A, (float*)G.b_qkv, st);
+        return colsum_acc(dt, n, 3 * A, rowp(B.dqkv, lr, 3 * A, e), 3 * A, (float*)G.b_qkv, ow, st);
       }));
     // LN1 backward + residual: dx = dx1 + LN1^T(du)
     void* out = li == 0 ? dx : rowp(S->lb[li - 1].dy, lr, H, e);
@@ -527,7 +536,7 @@ tp_status backward_impl(tp_stage* S, int l, int r, const void* dy, void* dx) {
     if (per_slice)
       TRY(launch(S, K_NORM, 0, 2 * nb, [&] {
         return ln_param_grads(dt, n, H, du, xin, mx, B.mean1 + lr, B.rstd1 + lr,
-                              (float*)G.ln1_g, (float*)G.ln1_b, st);
+                              (float*)G.ln1_g, (float*)G.ln1_b, ow, st);
       }));
     if (per_slice) {
       tp_status s = wgrad_gemms(S, li, lr, n);
@@ -605,8 +614,10 @@ void tp_stage_destroy(tp_stage* S) {
   delete S;
 }
 
-tp_status tp_kv_prefix_reset(tp_stage* S) {
-  if (!S) return TP_ERR_INVALID;
+tp_status tp_kv_prefix_reset(tp_stage* S) { return tp_kv_prefix_reset_ex(S, 0); }
+
+tp_status tp_kv_prefix_reset_ex(tp_stage* S, unsigned flags) {
+  if (!S || (flags & ~TP_SEQ_OVERWRITE_GRADS)) return TP_ERR_INVALID;
   const size_t n = (size_t)S->L * S->bsz * S->A;
   for (auto& B : S->lb) {
     TRY(fill_f32(B.dk, n, 0.f, S->stream));
@@ -616,6 +627,7 @@ tp_status tp_kv_prefix_reset(tp_stage* S) {
   S->cached_len = 0;
   S->bwd_frontier = 0;
   S->prepared = true;
+  S->grad_store = (flags & TP_SEQ_OVERWRITE_GRADS) != 0;
   return TP_OK;
 }
 
@@ -679,6 +691,8 @@ tp_status tp_slice_backward(tp_stage* S, int l, int r, const void* dy, void* dx)
   tp_status s = backward_impl(S, l, r, dy, dx);
   if (s != TP_OK) return s;
   S->bwd_frontier = l;
+  // every gradient has now been written once: later writes add
+  if (S->cfg.wgrad_mode == TP_WGRAD_PER_SLICE || l == 0) S->grad_store = false;
   return TP_OK;
 }
 
@@ -702,6 +716,7 @@ tp_status tp_profile_slice_cost(tp_stage* S, const int* lens, int n_lens, const 
   const bool was_timing = S->timing;
   S->timing = false;
   S->profiling = true;
+  S->grad_store = false;
   tp_status status = snapshot_wqkv(S) == hipSuccess ? TP_OK : TP_ERR_HIP;
   // deterministic, finite slice inputs
   const size_t io = (size_t)S->L * S->bsz * S->H;

@@ -25,7 +25,7 @@ template <typename T, int EPI>
 __device__ inline void epi1(const GemmArgs& a, int m, int n, float acc) {
   if constexpr (EPI == EPI_ACC_F32) {
     float* C = (float*)a.C + (long)m * a.ldc + n;
-    *C += acc;
+    *C = a.overwrite ? acc : *C + acc;
   } else if constexpr (EPI == EPI_DGELU) {
     const float z = ld((const T*)a.R + (long)m * a.ldr + n);
     st((T*)a.C + (long)m * a.ldc + n, acc * gelu_tanh_grad(z));
@@ -64,11 +64,15 @@ template <int EPI>
 __device__ inline void epi8(const GemmArgs& a, int m, int n, float* x) {
   if constexpr (EPI == EPI_ACC_F32) {
     float* c = (float*)a.C + (long)m * a.ldc + n;
-    float o[8];
-    ld8(c, o);
+    if (a.overwrite) {
+      st8(c, x);
+    } else {
+      float o[8];
+      ld8(c, o);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) o[i] += x[i];
-    st8(c, o);
+      for (int i = 0; i < 8; ++i) o[i] += x[i];
+      st8(c, o);
+    }
   } else if constexpr (EPI == EPI_DGELU) {
     float z[8];
     ld8((const bf16*)a.R + (long)m * a.ldr + n, z);

@@ -18,7 +18,8 @@ enum EpiKind {
   EPI_RESID = 2,  // C[m][n] = acc + bias[n] + R[m][n]
   EPI_GELU = 3,   // z = acc + bias[n]; C[m][n] = z; C2[m][n] = GELU(z)
   EPI_DGELU = 4,  // C[m][n] = acc * GELU'(R[m][n])
-  EPI_ACC_F32 = 5 // Cf[m][n] += acc (fp32 output, read-modify-write)
+  EPI_ACC_F32 = 5 // Cf[m][n] += acc (fp32 output, read-modify-write; with
+                  // GemmArgs::overwrite, Cf[m][n] = acc without the read)
 };
 
 struct GemmArgs {
@@ -46,6 +47,9 @@ struct GemmArgs {
   int qkv_f16 = 0;
   void* vb = nullptr;
   int r_f32 = 0, c_f32 = 0;
+  // EPI_ACC_F32 only: store acc instead of adding it (the destination's old
+  // contents are never read)
+  int overwrite = 0;
   // fp32 scratch for split-K partial sums (may be null: no split)
   float* ws = nullptr;
   long ws_elems = 0;
@@ -157,14 +161,16 @@ hipError_t ln_fwd(int dtype, int n, int H, const void* x, int x_f32, void* x_cop
 hipError_t ln_bwd(int dtype, int n, int H, const void* du, const void* x, int x_f32,
                   const float* mean, const float* rstd, const void* g, const void* resid, void* dx,
                   hipStream_t s);
-// dg[i] += sum_t du[t][i] * xhat[t][i];  db[i] += sum_t du[t][i]   (fp32 outputs)
+// dg[i] += sum_t du[t][i] * xhat[t][i];  db[i] += sum_t du[t][i]   (fp32 outputs;
+// with store set, = in place of +=)
 hipError_t ln_param_grads(int dtype, int n, int H, const void* du, const void* x, int x_f32,
-                          const float* mean, const float* rstd, float* dg, float* db,
+                          const float* mean, const float* rstd, float* dg, float* db, int store,
                           hipStream_t s);
 // dst[i] = fp16(src[i]) for n bf16 values (round to nearest even).
 hipError_t cvt_bf16_f16(size_t n, const void* src, void* dst, hipStream_t s);
-// out[j] += sum_{i<n} A[i*lda + j], j < N (fp32 output)
-hipError_t colsum_acc(int dtype, int n, int N, const void* A, long lda, float* out, hipStream_t s);
+// out[j] += sum_{i<n} A[i*lda + j], j < N (fp32 output; with store set, = in place of +=)
+hipError_t colsum_acc(int dtype, int n, int N, const void* A, long lda, float* out, int store,
+                      hipStream_t s);
 // dqkv[i][H + j] = dk[l+i][j], dqkv[i][2H + j] = dv[l+i][j] (stage dtype <- fp32)
 hipError_t pack_dkv(int dtype, int n, int H, const float* dk, const float* dv, void* dqkv,
                     hipStream_t s);

@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(HERE, "lib", "libterapipe.so")
 TP_OK, TP_ERR_INVALID, TP_ERR_ORDER, TP_ERR_UNSUPPORTED, TP_ERR_WORKSPACE, TP_ERR_HIP = (
     0, -1, -2, -3, -4, -5)
 DTYPE_BF16, DTYPE_FP32 = 0, 1
+SEQ_OVERWRITE_GRADS = 1
 WGRAD_PER_SLICE, WGRAD_DEFERRED = 0, 1
 
 PARAM_FIELDS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
@@ -28,7 +29,7 @@ SYNTH_NAMES = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
                "ln2_g", "ln2_b", "w1", "b1", "w2", "b2")
 
 EXPORTED = ("tp_stage_workspace_bytes", "tp_stage_init", "tp_stage_destroy",
-            "tp_kv_prefix_reset", "tp_slice_forward", "tp_slice_forward_static",
+            "tp_kv_prefix_reset", "tp_kv_prefix_reset_ex", "tp_slice_forward", "tp_slice_forward_static",
             "tp_slice_backward",
             "tp_profile_slice_cost", "tp_dp_optimal_slicing", "tp_dp_batch_split",
             "tp_dp_joint_slicing", "tp_fit_ctx_model",
@@ -74,6 +75,8 @@ def _load():
     lib.tp_stage_destroy.argtypes = [vp]
     lib.tp_kv_prefix_reset.restype = ctypes.c_int
     lib.tp_kv_prefix_reset.argtypes = [vp]
+    lib.tp_kv_prefix_reset_ex.restype = ctypes.c_int
+    lib.tp_kv_prefix_reset_ex.argtypes = [vp, ctypes.c_uint]
     for f in (lib.tp_slice_forward, lib.tp_slice_forward_static, lib.tp_slice_backward):
         f.restype = ctypes.c_int
         f.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, vp]
@@ -208,8 +211,14 @@ class Stage:
             for v in g.values():
                 v.zero_()
 
-    def reset(self):
-        _check(lib.tp_kv_prefix_reset(self._h), "tp_kv_prefix_reset")
+    def reset(self, overwrite_grads: bool = False):
+        """Start a sequence.  overwrite_grads: its gradients replace the buffers'
+        contents instead of adding to them (TP_SEQ_OVERWRITE_GRADS)."""
+        if overwrite_grads:
+            _check(lib.tp_kv_prefix_reset_ex(self._h, SEQ_OVERWRITE_GRADS),
+                   "tp_kv_prefix_reset_ex")
+        else:
+            _check(lib.tp_kv_prefix_reset(self._h), "tp_kv_prefix_reset")
 
     def _io(self, t: torch.Tensor, n: int) -> torch.Tensor:
         shape = (n, self.hidden) if self.batch == 1 else (n, self.batch, self.hidden)
@@ -241,12 +250,13 @@ class Stage:
         return dx
 
     def run_sequence(self, x: torch.Tensor, dy: torch.Tensor, fwd_lens: Sequence[int],
-                     bwd_lens: Optional[Sequence[int]] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+                     bwd_lens: Optional[Sequence[int]] = None,
+                     overwrite_grads: bool = False) -> Tuple[torch.Tensor, torch.Tensor]:
         """Reset, forward each slice in order, backward each slice in reverse."""
         L = x.shape[0]
         bwd_lens = list(fwd_lens) if bwd_lens is None else list(bwd_lens)
         assert sum(fwd_lens) == L and sum(bwd_lens) == L
-        self.reset()
+        self.reset(overwrite_grads)
         y = torch.empty_like(x)
         pos = 0
         for n in fwd_lens:

@@ -139,6 +139,20 @@ def test_slices_need_a_started_sequence():
         tp.lib.tp_stage_destroy(h)
 
 
+def test_reset_flags_checked_on_the_host():
+    """tp_kv_prefix_reset_ex refuses a null stage and unknown flag bits before
+    enqueuing anything."""
+    assert tp.lib.tp_kv_prefix_reset_ex(None, 0) == tp.TP_ERR_INVALID
+    assert tp.lib.tp_kv_prefix_reset_ex(None, tp.SEQ_OVERWRITE_GRADS) == tp.TP_ERR_INVALID
+    rc, h = _init(tp.make_config(1, 64, 4, 32, "bf16"))
+    assert rc == tp.TP_OK
+    for flags in (2, 4, 0x80000000, 0xFFFFFFFF):
+        assert tp.lib.tp_kv_prefix_reset_ex(h, flags) == tp.TP_ERR_INVALID
+    # still no sequence started
+    assert tp.lib.tp_slice_backward(h, 0, 8, 0x7e0000000000, 0x7e0000100000) == tp.TP_ERR_ORDER
+    tp.lib.tp_stage_destroy(h)
+
+
 def test_profile_argument_errors():
     cfg = tp.make_config(1, 64, 4, 32, "fp32")
     rc, h = _init(cfg)

@@ -54,6 +54,62 @@ def test_stored_ds_backward_head_width_64(wgrad):
           randomize_ln=True, label=f"d=64 stored dS {wgrad}")
 
 
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("wgrad", ["per_slice", "deferred"])
+def test_overwrite_grads_sequence(dtype, wgrad):
+    """tp_kv_prefix_reset_ex(TP_SEQ_OVERWRITE_GRADS): the sequence's gradients
+    replace NaN-filled buffers and equal those of zeroed buffers plus the
+    ordinary accumulating run (bit for bit on the bf16 matrix-core path, whose
+    dK/dV sums are ordered; within 1e-6 on the fp32 path, whose generic
+    attention backward adds with atomics), and match the oracle; a second
+    sequence started without the flag adds to them.  Two layers, hidden 384
+    (the 256 x 256 weight-gradient tiles end in half tiles), ragged slicings
+    (per-slice weight gradients over lengths off the 32-token grid)."""
+    from paper_2102_07988_amd import terapipe as tp
+    H, heads, L = 384, 3, 320
+    fwd, bwd = [100, 28, 192], [64, 37, 219]
+    params, x, dy = make_inputs(2, H, L, dtype, (11, 12, 13), randomize_ln=True)
+    _, x2, dy2 = make_inputs(2, H, L, dtype, (14, 12, 15))
+    dparams = [{k: v.cuda() for k, v in p.items()} for p in params]
+    st = tp.Stage(dparams, H, heads, L, dtype=dtype, wgrad=wgrad)
+    xd, dyd, x2d, dy2d = x.cuda(), dy.cuda(), x2.cuda(), dy2.cuda()
+
+    def grads():
+        return [{k: v.clone() for k, v in g.items()} for g in st.grads]
+
+    def same(a, b, what):
+        if dtype == "bf16":
+            assert torch.equal(a, b), what
+        else:
+            assert rel_l2(a.cpu().numpy(), b.cpu().numpy()) <= 1e-6, what
+
+    st.zero_grads()
+    y0, dx0 = st.run_sequence(xd, dyd, fwd, bwd)
+    g0 = grads()
+    st.run_sequence(x2d, dy2d, bwd, fwd)
+    g01 = grads()
+    for g in st.grads:
+        for v in g.values():
+            v.fill_(float("nan"))
+    y1, dx1 = st.run_sequence(xd, dyd, fwd, bwd, overwrite_grads=True)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y0)
+    same(dx1, dx0, "dx")
+    got = {"y": y1.float().cpu().numpy(), "dx": dx1.float().cpu().numpy(), "grads": []}
+    for li, (g, r) in enumerate(zip(st.grads, g0)):
+        got["grads"].append({k: v.cpu().numpy() for k, v in g.items()})
+        for k in g:
+            assert not torch.isnan(g[k]).any(), f"L{li}.{k} kept the NaN fill"
+            same(g[k], r[k], f"L{li}.{k} overwrite")
+    ref = run_oracle(params, x, dy, H, heads, L, fwd, bwd)
+    compare(got, ref, TOL[dtype], f"overwrite {dtype} {wgrad}")
+    st.run_sequence(x2d, dy2d, bwd, fwd)
+    torch.cuda.synchronize()
+    for li, (g, r) in enumerate(zip(st.grads, g01)):
+        for k in g:
+            same(g[k], r[k], f"L{li}.{k} accumulate after overwrite")
+
+
 def test_gpt3_13b_shape_reduced_sequence():
     """hidden 5120, 40 heads (d = 128), bf16, two slices of 16 after nothing cached."""
     _case(1, 5120, 40, 32, "bf16", [16, 16], label="13B-shape")
