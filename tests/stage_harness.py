@@ -28,12 +28,21 @@ def make_inputs(n_layers, H, L, dtype, seeds=(0, 1, 2), randomize_ln=False, op_p
     return params, x, dy
 
 
+def _nan_grads(st):
+    """Gradient buffers an overwriting sequence must never read."""
+    for g in st.grads:
+        for v in g.values():
+            v.fill_(float("nan"))
+
+
 def run_gpu(params, x, dy, H, heads, L, dtype, fwd_lens, bwd_lens=None, wgrad="per_slice",
-            device="cuda:0", op_parts=1):
+            device="cuda:0", op_parts=1, overwrite_grads=False):
     from paper_2102_07988_amd import terapipe as tp
     dparams = [{k: v.to(device).contiguous() for k, v in p.items()} for p in params]
     st = tp.Stage(dparams, H, heads, L, dtype=dtype, wgrad=wgrad, op_parts=op_parts)
-    y, dx = st.run_sequence(x.to(device), dy.to(device), fwd_lens, bwd_lens)
+    if overwrite_grads:
+        _nan_grads(st)
+    y, dx = st.run_sequence(x.to(device), dy.to(device), fwd_lens, bwd_lens, overwrite_grads)
     torch.cuda.synchronize()
     out = {"y": y.float().cpu().numpy(), "dx": dx.float().cpu().numpy(),
            "grads": [{k: v.cpu().numpy() for k, v in g.items()} for g in st.grads]}
@@ -61,13 +70,17 @@ def make_batch_inputs(n_layers, H, L, batch, dtype, seeds=(0, 1, 2), randomize_l
 
 
 def run_gpu_batch(params, x, dy, H, heads, L, dtype, fwd_lens, bwd_lens=None, wgrad="per_slice",
-                  device="cuda:0", op_parts=1):
-    """One batched stage (batch = x.shape[1]) over the whole sequence."""
+                  device="cuda:0", op_parts=1, overwrite_grads=False):
+    """One batched stage (batch = x.shape[1]) over the whole sequence; with
+    overwrite_grads the gradient buffers start NaN-filled and the sequence
+    stores its gradients (TP_SEQ_OVERWRITE_GRADS)."""
     from paper_2102_07988_amd import terapipe as tp
     dparams = [{k: v.to(device).contiguous() for k, v in p.items()} for p in params]
     st = tp.Stage(dparams, H, heads, L, dtype=dtype, wgrad=wgrad, batch=x.shape[1],
                   op_parts=op_parts)
-    y, dx = st.run_sequence(x.to(device), dy.to(device), fwd_lens, bwd_lens)
+    if overwrite_grads:
+        _nan_grads(st)
+    y, dx = st.run_sequence(x.to(device), dy.to(device), fwd_lens, bwd_lens, overwrite_grads)
     torch.cuda.synchronize()
     out = {"y": y.float().cpu().numpy(), "dx": dx.float().cpu().numpy(),
            "grads": [{k: v.cpu().numpy() for k, v in g.items()} for g in st.grads]}

@@ -15,11 +15,12 @@ TOL = {"fp32": 1e-4, "bf16": 2e-2}
 
 
 def _case(n_layers, H, heads, L, b, dtype, fwd, bwd=None, wgrad="per_slice", seeds=(0, 1, 2),
-          randomize_ln=False, label=""):
+          randomize_ln=False, label="", overwrite=False):
     print(f"case {label}: layers={n_layers} H={H} heads={heads} L={L} batch={b} {dtype} "
-          f"{wgrad} fwd={fwd} bwd={bwd}", flush=True)
+          f"{wgrad} fwd={fwd} bwd={bwd} overwrite={overwrite}", flush=True)
     params, x, dy = make_batch_inputs(n_layers, H, L, b, dtype, seeds, randomize_ln)
-    got = run_gpu_batch(params, x, dy, H, heads, L, dtype, fwd, bwd, wgrad)
+    got = run_gpu_batch(params, x, dy, H, heads, L, dtype, fwd, bwd, wgrad,
+                        overwrite_grads=overwrite)
     ref = run_oracle_batch(params, x, dy, H, heads, L, fwd, bwd)
     return compare(got, ref, TOL[dtype], label)
 
@@ -37,6 +38,15 @@ def test_matrix_core_batch_ragged(H, heads, wgrad):
     """Three sequences, ragged forward slices and different backward slices."""
     _case(2, H, heads, 150, 3, "bf16", [37, 1, 29, 83], [50, 7, 93], wgrad, seeds=(11, 12, 13),
           randomize_ln=True, label=f"mfma-attn d={H // heads} b=3")
+
+
+@pytest.mark.parametrize("wgrad", ["per_slice", "deferred"])
+def test_batch_overwrite_grads(wgrad):
+    """Three sequences whose batch stores its gradients over NaN-filled buffers
+    (TP_SEQ_OVERWRITE_GRADS): the sum of the sequences' gradients, as the
+    oracle gives it."""
+    _case(2, 256, 2, 150, 3, "bf16", [37, 1, 29, 83], [50, 7, 93], wgrad, seeds=(14, 15, 16),
+          randomize_ln=True, label=f"b=3 overwrite {wgrad}", overwrite=True)
 
 
 def test_batch_long_backward_slice_in_query_chunks():

@@ -18,8 +18,9 @@ more), unsplit d = 128 dQ launches.
   measured on this GPU at the paper's pipeline depth K = 20, slice lengths in
   multiples of 16; and per-slice weight gradients with another backward slicing.
 * GPT-3-175B stage (2 layers, 2048 tokens): the benchmark's 8 x 256 with
-  deferred weight gradients, the DP slicing at K = 48, and per-slice weight
-  gradients with 4 x 512 backward slices.
+  deferred weight gradients stored over NaN-filled buffers (as the benchmark
+  runs it), the DP slicing at K = 48, and per-slice weight gradients with
+  4 x 512 backward slices.
 * One GPU's shard of the paper's 175B settings with operation partitioning
   (Table 1 settings (10) and (9)): 8-way (2 layers) and 4-way (1 layer).
 * Hidden 11136 (87 heads), whose query/key/value product runs as two split
@@ -98,12 +99,19 @@ def dp_slicing(params, H, heads, L, K, unit, op_parts=1):
     return lens
 
 
-def check_run(ref, params, x, dy, H, heads, L, dtype, fwd, bwd, wgrad, label, op_parts=1):
+def check_run(ref, params, x, dy, H, heads, L, dtype, fwd, bwd, wgrad, label, op_parts=1,
+              overwrite=False):
+    """overwrite: the gradient buffers start NaN-filled and the sequence stores
+    its gradients (TP_SEQ_OVERWRITE_GRADS, as the benchmark runs it)."""
     from paper_2102_07988_amd import terapipe as tp
     log(f"case {label}: H={H} heads={heads} L={L} {dtype} {wgrad} op_parts={op_parts} "
-        f"fwd={fwd} bwd={bwd}")
+        f"fwd={fwd} bwd={bwd} overwrite={overwrite}")
     st = tp.Stage(params, H, heads, L, dtype=dtype, wgrad=wgrad, op_parts=op_parts)
-    y, dx = st.run_sequence(x, dy, fwd, bwd)
+    if overwrite:
+        for g in st.grads:
+            for v in g.values():
+                v.fill_(float("nan"))
+    y, dx = st.run_sequence(x, dy, fwd, bwd, overwrite_grads=overwrite)
     torch.cuda.synchronize()
     errs = {"y": rel_l2(y.cpu(), ref["y"]), "dx": rel_l2(dx.cpu(), ref["dx"])}
     del y, dx
@@ -150,7 +158,7 @@ def test_175b_stage_full_sequence():
     lens = dp_slicing(params, H, heads, L, K=48, unit=16)
     ref = oracle(params, x, dy, heads)
     check_run(ref, params, x, dy, H, heads, L, "bf16", [256] * 8, None, "deferred",
-              "175B stage, benchmark configuration 8 x 256")
+              "175B stage, benchmark configuration 8 x 256, gradients stored", overwrite=True)
     check_run(ref, params, x, dy, H, heads, L, "bf16", lens, None, "deferred",
               "175B stage, DP slicing")
     check_run(ref, params, x, dy, H, heads, L, "bf16", [256] * 8, [512] * 4, "per_slice",

@@ -48,12 +48,14 @@ def test_shard_stored_ds_backward(wgrad):
           label=f"shard p=2 stored dS {wgrad}")
 
 
-def test_shard_with_batch():
+@pytest.mark.parametrize("overwrite", [False, True])
+def test_shard_with_batch(overwrite):
     """Operation partitioning and batch slices together (setting (10) of Table 1
-    has both): two sequences through an 8-way shard."""
+    has both): two sequences through an 8-way shard; also with the gradients
+    stored over NaN-filled buffers (TP_SEQ_OVERWRITE_GRADS)."""
     H, heads, p, L = 1024, 8, 8, 96
     params, x, dy = make_batch_inputs(2, H, L, 2, "bf16", (7, 8, 9), True, op_parts=p)
     got = run_gpu_batch(params, x, dy, H, heads, L, "bf16", [40, 56], [64, 32], "deferred",
-                        op_parts=p)
+                        op_parts=p, overwrite_grads=overwrite)
     ref = run_oracle_batch(params, x, dy, H, heads, L, [40, 56], [64, 32], op_parts=p)
-    compare(got, ref, TOL["bf16"], "shard p=8 batch 2")
+    compare(got, ref, TOL["bf16"], f"shard p=8 batch 2 overwrite={overwrite}")
