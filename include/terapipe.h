@@ -208,7 +208,9 @@ tp_status tp_slice_forward_static(tp_stage *stage, int l, int r, const void *x, 
  * the backward frontier (slices arrive in reverse order; their boundaries need
  * not match the forward slicing) in a sequence started by tp_kv_prefix_reset,
  * else TP_ERR_ORDER / TP_ERR_INVALID (argument checks come first).  Adds
- * this slice's contributions to the parameter gradients; the gradient that
+ * this slice's contributions to the parameter gradients (stores them where
+ * the sequence started with TP_SEQ_OVERWRITE_GRADS and this is its first
+ * gradient write, see tp_kv_prefix_reset_ex); the gradient that
  * queries in [l, r) send to earlier keys/values is added to the dK/dV buffer.
  * Sets the frontier to l; in DEFERRED mode the weight-gradient GEMMs run when
  * l reaches 0.  dy and dx must not overlap and must be 16-byte aligned. */
