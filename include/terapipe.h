@@ -226,7 +226,8 @@ tp_status tp_slice_backward(tp_stage *stage, int l, int r, const void *dy, void 
  * and bias / LayerNorm-parameter reductions.
  * Synchronous.  Overwrites the K/V cache, the arenas and the parameter
  * gradients with meaningless values and ends any sequence: slice calls return
- * TP_ERR_ORDER until tp_kv_prefix_reset; zero the gradients afterwards. */
+ * TP_ERR_ORDER until tp_kv_prefix_reset; zero the gradients afterwards (or
+ * start the next sequence with TP_SEQ_OVERWRITE_GRADS). */
 tp_status tp_profile_slice_cost(tp_stage *stage, const int *lens, int n_lens, const int *ctxs,
                                 int n_ctxs, int warmup, int reps, int64_t *t_fwd_ns,
                                 int64_t *t_bwd_ns);
