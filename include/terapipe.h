@@ -149,6 +149,7 @@ tp_status tp_kv_prefix_reset(tp_stage *stage);
 
 /* Flags of tp_kv_prefix_reset_ex. */
 #define TP_SEQ_OVERWRITE_GRADS 1u
+#define TP_SEQ_REUSE_WQKV_COPY 2u
 
 /* tp_kv_prefix_reset, plus per-sequence flags (0 = tp_kv_prefix_reset).
  * TP_SEQ_OVERWRITE_GRADS: the sequence's first write of each parameter
@@ -164,6 +165,14 @@ tp_status tp_kv_prefix_reset(tp_stage *stage);
  * the same gradients as whole-sequence processing); it saves the read of
  * every fp32 gradient in the weight-gradient GEMMs' epilogues and the
  * caller's zeroing pass.
+ * TP_SEQ_REUSE_WQKV_COPY (mixed-precision path, see Conventions; no effect
+ * elsewhere): W_qkv is unchanged since the fp16 copy was last taken (by the
+ * previous sequence start or profiling call on this stage), so that copy is
+ * kept instead of converting W_qkv again; with no copy taken yet it is taken.
+ * For the later sequences or batch slices (Sec. 3.4) of one training
+ * iteration, which all use the same weights.  The caller vouches for it: after
+ * W_qkv has changed, the forward's query/key/value product would run on the
+ * old weights.
  * Errors: TP_ERR_INVALID (null stage, unknown flag bits; nothing enqueued),
  * TP_ERR_HIP. */
 tp_status tp_kv_prefix_reset_ex(tp_stage *stage, unsigned flags);

@@ -94,6 +94,8 @@ struct tp_stage {
   // the sequence's next gradient writes store rather than add
   // (TP_SEQ_OVERWRITE_GRADS; cleared once every gradient has been written)
   bool grad_store = false;
+  // the fp16 W_qkv copies hold the current weights as of the last snapshot
+  bool w16_valid = false;
   bool profiling = false;
   // planning pass (tp_slice_forward_static): no launch, only the largest
   // partial-sum scratch (fp32 elements) the slice's kernels would take
@@ -369,6 +371,7 @@ tp_status deferred_param_reductions(tp_stage* S, int li, int rows) {
 // query/key/value product, taken at the start of a sequence (the parameters
 // stay fixed while its slices run).
 hipError_t snapshot_wqkv(tp_stage* S) {
+  S->w16_valid = false;
   if (!S->mixed) return hipSuccess;
   const size_t n = (size_t)3 * S->A * S->H;
   for (int li = 0; li < S->cfg.n_layers; ++li) {
@@ -376,6 +379,7 @@ hipError_t snapshot_wqkv(tp_stage* S) {
                                 [&] { return cvt_bf16_f16(n, S->P[li].w_qkv, S->lb[li].w16, S->stream); });
     if (e != hipSuccess) return e;
   }
+  S->w16_valid = true;
   return hipSuccess;
 }
 
@@ -617,13 +621,13 @@ void tp_stage_destroy(tp_stage* S) {
 tp_status tp_kv_prefix_reset(tp_stage* S) { return tp_kv_prefix_reset_ex(S, 0); }
 
 tp_status tp_kv_prefix_reset_ex(tp_stage* S, unsigned flags) {
-  if (!S || (flags & ~TP_SEQ_OVERWRITE_GRADS)) return TP_ERR_INVALID;
+  if (!S || (flags & ~(TP_SEQ_OVERWRITE_GRADS | TP_SEQ_REUSE_WQKV_COPY))) return TP_ERR_INVALID;
   const size_t n = (size_t)S->L * S->bsz * S->A;
   for (auto& B : S->lb) {
     TRY(fill_f32(B.dk, n, 0.f, S->stream));
     TRY(fill_f32(B.dv, n, 0.f, S->stream));
   }
-  TRY(snapshot_wqkv(S));
+  if (!(flags & TP_SEQ_REUSE_WQKV_COPY) || !S->w16_valid) TRY(snapshot_wqkv(S));
   S->cached_len = 0;
   S->bwd_frontier = 0;
   S->prepared = true;

@@ -20,6 +20,7 @@ TP_OK, TP_ERR_INVALID, TP_ERR_ORDER, TP_ERR_UNSUPPORTED, TP_ERR_WORKSPACE, TP_ER
     0, -1, -2, -3, -4, -5)
 DTYPE_BF16, DTYPE_FP32 = 0, 1
 SEQ_OVERWRITE_GRADS = 1
+SEQ_REUSE_WQKV_COPY = 2
 WGRAD_PER_SLICE, WGRAD_DEFERRED = 0, 1
 
 PARAM_FIELDS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
@@ -211,12 +212,15 @@ class Stage:
             for v in g.values():
                 v.zero_()
 
-    def reset(self, overwrite_grads: bool = False):
+    def reset(self, overwrite_grads: bool = False, reuse_wqkv_copy: bool = False):
         """Start a sequence.  overwrite_grads: its gradients replace the buffers'
-        contents instead of adding to them (TP_SEQ_OVERWRITE_GRADS)."""
-        if overwrite_grads:
-            _check(lib.tp_kv_prefix_reset_ex(self._h, SEQ_OVERWRITE_GRADS),
-                   "tp_kv_prefix_reset_ex")
+        contents instead of adding to them (TP_SEQ_OVERWRITE_GRADS);
+        reuse_wqkv_copy: W_qkv is unchanged, keep its fp16 copy
+        (TP_SEQ_REUSE_WQKV_COPY)."""
+        flags = ((SEQ_OVERWRITE_GRADS if overwrite_grads else 0) |
+                 (SEQ_REUSE_WQKV_COPY if reuse_wqkv_copy else 0))
+        if flags:
+            _check(lib.tp_kv_prefix_reset_ex(self._h, flags), "tp_kv_prefix_reset_ex")
         else:
             _check(lib.tp_kv_prefix_reset(self._h), "tp_kv_prefix_reset")
 

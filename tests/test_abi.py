@@ -146,7 +146,7 @@ def test_reset_flags_checked_on_the_host():
     assert tp.lib.tp_kv_prefix_reset_ex(None, tp.SEQ_OVERWRITE_GRADS) == tp.TP_ERR_INVALID
     rc, h = _init(tp.make_config(1, 64, 4, 32, "bf16"))
     assert rc == tp.TP_OK
-    for flags in (2, 4, 0x80000000, 0xFFFFFFFF):
+    for flags in (4, 5, 0x80000000, 0xFFFFFFFF):
         assert tp.lib.tp_kv_prefix_reset_ex(h, flags) == tp.TP_ERR_INVALID
     # still no sequence started
     assert tp.lib.tp_slice_backward(h, 0, 8, 0x7e0000000000, 0x7e0000100000) == tp.TP_ERR_ORDER

@@ -110,6 +110,47 @@ def test_overwrite_grads_sequence(dtype, wgrad):
             same(g[k], r[k], f"L{li}.{k} accumulate after overwrite")
 
 
+def test_reused_wqkv_copy():
+    """tp_kv_prefix_reset_ex(TP_SEQ_REUSE_WQKV_COPY) on the mixed-precision path:
+    with W_qkv unchanged a sequence gives bit for bit what a full reset gives;
+    after W_qkv changes, the flag keeps the forward's query/key/value product
+    on the copy of the old weights (outputs as before the change) while a full
+    reset converts the new weights."""
+    from paper_2102_07988_amd import terapipe as tp
+    H, heads, L = 256, 2, 96  # d = 128: fp16 scores and W_qkv copy
+    fwd, bwd = [40, 56], [64, 32]
+    params, x, dy = make_inputs(2, H, L, "bf16", (21, 22, 23), randomize_ln=True)
+    dparams = [{k: v.cuda() for k, v in p.items()} for p in params]
+    st = tp.Stage(dparams, H, heads, L, dtype="bf16", wgrad="deferred")
+    xd, dyd = x.cuda(), dy.cuda()
+    y0, dx0 = st.run_sequence(xd, dyd, fwd, bwd, overwrite_grads=True)
+    g0 = [{k: v.clone() for k, v in g.items()} for g in st.grads]
+    st.reset(overwrite_grads=True, reuse_wqkv_copy=True)
+    y1, dx1 = torch.empty_like(xd), torch.empty_like(dyd)
+    for l, r in [(0, 40), (40, 96)]:
+        st.forward(l, r, xd[l:r], out=y1[l:r])
+    for l, r in [(64, 96), (0, 64)]:
+        st.backward(l, r, dyd[l:r], out=dx1[l:r])
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y0) and torch.equal(dx1, dx0)
+    for g, r in zip(st.grads, g0):
+        for k in g:
+            assert torch.equal(g[k], r[k]), k
+    with torch.no_grad():
+        dparams[0]["w_qkv"].mul_(0.5)
+    y2 = torch.empty_like(xd)
+    st.reset(reuse_wqkv_copy=True)
+    for l, r in [(0, 40), (40, 96)]:
+        st.forward(l, r, xd[l:r], out=y2[l:r])
+    torch.cuda.synchronize()
+    assert torch.equal(y2, y0)
+    st.reset()
+    for l, r in [(0, 40), (40, 96)]:
+        st.forward(l, r, xd[l:r], out=y2[l:r])
+    torch.cuda.synchronize()
+    assert not torch.equal(y2, y0)
+
+
 def test_gpt3_13b_shape_reduced_sequence():
     """hidden 5120, 40 heads (d = 128), bf16, two slices of 16 after nothing cached."""
     _case(1, 5120, 40, 32, "bf16", [16, 16], label="13B-shape")
