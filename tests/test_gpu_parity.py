@@ -151,6 +151,50 @@ def test_reused_wqkv_copy():
     assert not torch.equal(y2, y0)
 
 
+def _random_slicing(rng, L, max_len):
+    lens = []
+    while sum(lens) < L:
+        lens.append(int(min(rng.integers(1, max_len + 1), L - sum(lens))))
+    return lens
+
+
+@pytest.mark.parametrize("heads", [2, 4])  # d = 128, 64: the matrix-core attention kernels
+def test_random_slicings_against_one_oracle_run(heads):
+    """Twelve seeded random forward and backward slicings (lengths 1..200, so
+    slice boundaries fall anywhere relative to the 32-, 64-, 128- and 256-row
+    blocks of every kernel), alternating weight-gradient modes and gradient
+    buffer modes, all against one whole-sequence oracle run (the oracle is
+    slicing-invariant bit for bit)."""
+    from paper_2102_07988_amd import terapipe as tp
+    H, L = 256, 600
+    params, x, dy = make_inputs(2, H, L, "bf16", (61, 62, 63), randomize_ln=True)
+    ref = run_oracle(params, x, dy, H, heads, L, [L])
+    rng = np.random.default_rng(2102)
+    dparams = [{k: v.cuda() for k, v in p.items()} for p in params]
+    xd, dyd = x.cuda(), dy.cuda()
+    stages = {w: tp.Stage(dparams, H, heads, L, dtype="bf16", wgrad=w)
+              for w in ("per_slice", "deferred")}
+    for case in range(12):
+        fwd = _random_slicing(rng, L, 200)
+        bwd = _random_slicing(rng, L, 200)
+        wgrad = ("per_slice", "deferred")[case % 2]
+        overwrite = case % 4 >= 2
+        st = stages[wgrad]
+        print(f"case {case}: heads={heads} {wgrad} overwrite={overwrite} fwd={fwd} bwd={bwd}",
+              flush=True)
+        if overwrite:
+            for g in st.grads:
+                for v in g.values():
+                    v.fill_(float("nan"))
+        else:
+            st.zero_grads()
+        y, dx = st.run_sequence(xd, dyd, fwd, bwd, overwrite_grads=overwrite)
+        torch.cuda.synchronize()
+        got = {"y": y.float().cpu().numpy(), "dx": dx.float().cpu().numpy(),
+               "grads": [{k: v.cpu().numpy() for k, v in g.items()} for g in st.grads]}
+        compare(got, ref, TOL["bf16"], f"random slicing {case}")
+
+
 def test_gpt3_13b_shape_reduced_sequence():
     """hidden 5120, 40 heads (d = 128), bf16, two slices of 16 after nothing cached."""
     _case(1, 5120, 40, 32, "bf16", [16, 16], label="13B-shape")
