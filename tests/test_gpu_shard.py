@@ -3,6 +3,7 @@ column): heads / p heads and 4H / p FFN units on the full residual stream,
 checked against the shard oracle (itself pinned bit for bit to the full-width
 oracle on zero-embedded weights) on the same seeded inputs."""
 import pytest
+import torch
 
 from stage_harness import (compare, make_batch_inputs, make_inputs, run_gpu, run_gpu_batch,
                            run_oracle, run_oracle_batch)
@@ -59,3 +60,44 @@ def test_shard_with_batch(overwrite):
                         op_parts=p, overwrite_grads=overwrite)
     ref = run_oracle_batch(params, x, dy, H, heads, L, [40, 56], [64, 32], op_parts=p)
     compare(got, ref, TOL["bf16"], f"shard p=8 batch 2 overwrite={overwrite}")
+
+
+def test_random_slicings_shard_with_batch():
+    """Eight seeded random forward and backward slicings (lengths 1..160) of
+    two sequences through a 2-way shard (2 local heads of d = 128 on a 512
+    residual), alternating weight-gradient and gradient-buffer modes, against
+    one oracle run per sequence (gradients summed)."""
+    import numpy as np
+    from paper_2102_07988_amd import terapipe as tp
+    H, heads, p, L, b = 512, 4, 2, 400, 2
+    params, x, dy = make_batch_inputs(2, H, L, b, "bf16", (71, 72, 73), True, op_parts=p)
+    ref = run_oracle_batch(params, x, dy, H, heads, L, [L], op_parts=p)
+    rng = np.random.default_rng(3402)
+    dparams = [{k: v.cuda() for k, v in q.items()} for q in params]
+    xd, dyd = x.cuda(), dy.cuda()
+    stages = {w: tp.Stage(dparams, H, heads, L, dtype="bf16", wgrad=w, batch=b, op_parts=p)
+              for w in ("per_slice", "deferred")}
+
+    def slicing():
+        lens = []
+        while sum(lens) < L:
+            lens.append(int(min(rng.integers(1, 161), L - sum(lens))))
+        return lens
+
+    for case in range(8):
+        fwd, bwd = slicing(), slicing()
+        wgrad = ("per_slice", "deferred")[case % 2]
+        overwrite = case % 4 >= 2
+        st = stages[wgrad]
+        print(f"case {case}: {wgrad} overwrite={overwrite} fwd={fwd} bwd={bwd}", flush=True)
+        if overwrite:
+            for g in st.grads:
+                for v in g.values():
+                    v.fill_(float("nan"))
+        else:
+            st.zero_grads()
+        y, dx = st.run_sequence(xd, dyd, fwd, bwd, overwrite_grads=overwrite)
+        torch.cuda.synchronize()
+        got = {"y": y.float().cpu().numpy(), "dx": dx.float().cpu().numpy(),
+               "grads": [{k: v.cpu().numpy() for k, v in g.items()} for g in st.grads]}
+        compare(got, ref, TOL["bf16"], f"shard p=2 batch 2 random slicing {case}")
