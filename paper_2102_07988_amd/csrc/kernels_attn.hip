@@ -967,35 +967,61 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_stream(AttnArgs a0) {
 
 // ------------------------------------------------------ split combines
 
+// At most MAX_SPLIT key-range splits per launch (plan_split).
+constexpr int MAX_SPLIT = 8;
+
 // Forward: one wave per (row, head) merges the splits' partials in split
 // order: M = max_z m_z, L = sum_z l_z 2^(m_z - M), O = sum_z O_z 2^(m_z - M) / L.
+// Every load (each split's (m, l) pair and its D / 64 partial values per
+// lane) is issued before the first use, so the wave waits for memory once.
 template <int D>
 __global__ __launch_bounds__(256) void attn_fwd_combine(AttnArgs a) {
+  constexpr int PER = D / 64;  // consecutive columns per lane
+  static_assert(PER == 1 || PER == 2, "head width 64 or 128");
   const int n = a.r - a.l, lane = threadIdx.x & 63;
   const long rows = (long)n * a.bs, wave = ((long)blockIdx.x * 256 + threadIdx.x) >> 6;
   if (wave >= rows * a.heads) return;
   const int i = (int)(wave / a.heads), h = (int)(wave % a.heads);  // row i = (t - l) bs + s
   const int tl = i / a.bs, s = i % a.bs;
   const long plane = rows * a.H;
-  const float* part = a.ws + (long)i * a.H + h * D;
+  const float* part = a.ws + (long)i * a.H + h * D + PER * lane;
   const float* ml = a.ws + a.nsplit * plane + (((long)s * a.heads + h) * n + tl) * 2;
   const long ml_split = (long)a.bs * a.heads * n * 2;
-  float M = -INFINITY;
-  for (int z = 0; z < a.nsplit; ++z) M = fmaxf(M, ml[z * ml_split]);
-  // weight of split z (0 for a split that saw no key of this query)
-  auto fz = [&](int z) {
-    const float mz = ml[z * ml_split];
-    return mz == -INFINITY ? 0.f : exp2_fast(mz - M);
-  };
-  float L = 0.f;
-  for (int z = 0; z < a.nsplit; ++z) L += ml[z * ml_split + 1] * fz(z);
-  const float inv = L > 0.f ? 1.f / L : 0.f;
-  uint16_t* O = (uint16_t*)a.o + (long)i * a.H + h * D;
-  for (int j = lane; j < D; j += 64) {
-    float acc = 0.f;
-    for (int z = 0; z < a.nsplit; ++z) acc += part[z * plane + j] * fz(z);
-    O[j] = f32_to_bf16_bits(acc * inv);
+  float m[MAX_SPLIT], l[MAX_SPLIT], v[MAX_SPLIT][PER];
+#pragma unroll
+  for (int z = 0; z < MAX_SPLIT; ++z) {
+    if (z < a.nsplit) {
+      const float2 t = *(const float2*)(ml + z * ml_split);
+      m[z] = t.x, l[z] = t.y;
+      if constexpr (PER == 2) {
+        const float2 u = *(const float2*)(part + z * plane);
+        v[z][0] = u.x, v[z][1] = u.y;
+      } else {
+        v[z][0] = part[z * plane];
+      }
+    }
   }
+  float M = -INFINITY;
+#pragma unroll
+  for (int z = 0; z < MAX_SPLIT; ++z)
+    if (z < a.nsplit) M = fmaxf(M, m[z]);
+  // weight of split z (0 for a split that saw no key of this query)
+  float L = 0.f, acc[PER] = {};
+#pragma unroll
+  for (int z = 0; z < MAX_SPLIT; ++z) {
+    if (z < a.nsplit) {
+      const float f = m[z] == -INFINITY ? 0.f : exp2_fast(m[z] - M);
+      L += l[z] * f;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) acc[e] += v[z][e] * f;
+    }
+  }
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+  uint16_t* O = (uint16_t*)a.o + (long)i * a.H + h * D + PER * lane;
+  if constexpr (PER == 2)
+    *(uint32_t*)O = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+  else
+    O[0] = f32_to_bf16_bits(acc[0] * inv);
   if (lane == 0) a.lse[((long)s * a.heads + h) * a.Lmax + a.l + tl] = (M + log2f(L)) * LN2;
 }
 
@@ -1024,7 +1050,6 @@ __global__ __launch_bounds__(256) void attn_dq_combine(AttnArgs a) {
 }
 
 constexpr int NWF = 4;  // waves per block
-constexpr int MAX_SPLIT = 8;
 
 // Key-range splits for a query-parallel launch that fills under half of the
 // 256 CUs: enough splits for about one block per CU, at most MAX_SPLIT, each
