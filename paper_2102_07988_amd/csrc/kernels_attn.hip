@@ -1034,11 +1034,21 @@ __global__ __launch_bounds__(256) void attn_dq_combine(AttnArgs a) {
   const long i = e / a8, col = (e - i * a8) * 8;
   const long plane = rows * a.H;
   float acc[8] = {};
-  for (int z = 0; z < a.nsplit; ++z) {
-    const float4* p = (const float4*)(a.ws + z * plane + i * a.H + col);
-    const float4 u = p[0], w = p[1];
-    acc[0] += u.x, acc[1] += u.y, acc[2] += u.z, acc[3] += u.w;
-    acc[4] += w.x, acc[5] += w.y, acc[6] += w.z, acc[7] += w.w;
+  // every split's values in flight before the first add (at most MAX_SPLIT)
+  float4 u[MAX_SPLIT], w[MAX_SPLIT];
+#pragma unroll
+  for (int z = 0; z < MAX_SPLIT; ++z) {
+    if (z < a.nsplit) {
+      const float4* p = (const float4*)(a.ws + z * plane + i * a.H + col);
+      u[z] = p[0], w[z] = p[1];
+    }
+  }
+#pragma unroll
+  for (int z = 0; z < MAX_SPLIT; ++z) {
+    if (z < a.nsplit) {
+      acc[0] += u[z].x, acc[1] += u[z].y, acc[2] += u[z].z, acc[3] += u[z].w;
+      acc[4] += w[z].x, acc[5] += w[z].y, acc[6] += w[z].z, acc[7] += w[z].w;
+    }
   }
   uint16_t* dst = (uint16_t*)a.dq + (i / a.bs) * a.ld_dq + (i % a.bs) * a.dq_seq + col;
   uint4 o;

@@ -273,11 +273,25 @@ __global__ __launch_bounds__(256) void splitk_reduce8_kernel(GemmArgs a) {
     // split_cols is a multiple of 8: the 8 columns lie in one group
     const SplitPlanes sp = split_planes(a, n);
     float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int z = 0; z < sp.count; ++z) {
-      const float4* p = (const float4*)(sp.p + z * sp.plane + (long)m * sp.ld);
-      const float4 u = p[0], w = p[1];
-      s[0] += u.x, s[1] += u.y, s[2] += u.z, s[3] += u.w;
-      s[4] += w.x, s[5] += w.y, s[6] += w.z, s[7] += w.w;
+    // RED planes' loads in flight before the first add (one memory round trip
+    // per RED splits, not per split); the adds stay in split order
+    constexpr int RED = 4;
+    for (int z0 = 0; z0 < sp.count; z0 += RED) {
+      float4 u[RED], w[RED];
+#pragma unroll
+      for (int k = 0; k < RED; ++k) {
+        if (z0 + k < sp.count) {
+          const float4* p = (const float4*)(sp.p + (z0 + k) * sp.plane + (long)m * sp.ld);
+          u[k] = p[0], w[k] = p[1];
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < RED; ++k) {
+        if (z0 + k < sp.count) {
+          s[0] += u[k].x, s[1] += u[k].y, s[2] += u[k].z, s[3] += u[k].w;
+          s[4] += w[k].x, s[5] += w[k].y, s[6] += w[k].z, s[7] += w[k].w;
+        }
+      }
     }
     epi8<EPI>(a, m, n, s);
   }
