@@ -153,6 +153,21 @@ def test_reset_flags_checked_on_the_host():
     tp.lib.tp_stage_destroy(h)
 
 
+def test_header_constants_match_the_binding():
+    """The #define and enum values of include/terapipe.h are the binding's."""
+    src = open(os.path.join(ROOT, "include", "terapipe.h")).read()
+    defines = dict((k, int(v.rstrip("u"), 0)) for k, v in
+                   re.findall(r"#define\s+(TP_\w+)\s+(\w+)", src) if k != "TERAPIPE_H")
+    assert defines == {"TP_SEQ_OVERWRITE_GRADS": tp.SEQ_OVERWRITE_GRADS,
+                       "TP_SEQ_REUSE_WQKV_COPY": tp.SEQ_REUSE_WQKV_COPY}
+    enums = dict((k, int(v)) for k, v in re.findall(r"\b(TP_[A-Z0-9_]+)\s*=\s*(-?\d+)", src))
+    assert enums["TP_OK"] == tp.TP_OK and enums["TP_ERR_HIP"] == tp.TP_ERR_HIP
+    assert enums["TP_ERR_ORDER"] == tp.TP_ERR_ORDER
+    assert enums["TP_DTYPE_BF16"] == tp.DTYPE_BF16 and enums["TP_DTYPE_FP32"] == tp.DTYPE_FP32
+    assert enums["TP_WGRAD_PER_SLICE"] == tp.WGRAD_PER_SLICE
+    assert enums["TP_WGRAD_DEFERRED"] == tp.WGRAD_DEFERRED
+
+
 def test_profile_argument_errors():
     cfg = tp.make_config(1, 64, 4, 32, "fp32")
     rc, h = _init(cfg)
