@@ -63,6 +63,8 @@ __device__ inline int swz_mc(int k) {
   else return (k & 3) << 2;
 }
 
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+
 __device__ inline void dma16(const uint16_t* g, uint16_t* lds_wave_base) {
   __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
                                    (__attribute__((address_space(3))) void*)lds_wave_base, 16, 0,
@@ -450,7 +452,15 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_dma_kernel(GemmArgs a) {
             const float4 o = pre[t % P][q];
             x[q].x += o.x, x[q].y += o.y, x[q].z += o.z, x[q].w += o.w;
           }
-          *(float4*)dst_of(t, q) = x[q];
+          if constexpr (SPLIT) {
+            *(float4*)dst_of(t, q) = x[q];
+          } else {
+            // the fp32 weight gradient is not read again by this sequence's
+            // kernels: a non-temporal store keeps it from displacing their
+            // operands in the caches
+            const f32x4v v = {x[q].x, x[q].y, x[q].z, x[q].w};
+            __builtin_nontemporal_store(v, (f32x4v*)dst_of(t, q));
+          }
         }
         if (add && t + P < T) {
 #pragma unroll
