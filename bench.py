@@ -51,7 +51,7 @@ PEAK_HBM_GBS = 8000.0
 TRAFFIC = {
     "gemm_bwd_dw_tn": {"workload": "gpt3-175b-stage", "grad_buffers": "overwrite",
                        "source": "paper_2102_07988_amd/csrc/kernels_gemm_dma.hip",
-                       "sha256_16": "a97547c36515da7b", "bytes_per_launch": 4549985731},
+                       "sha256_16": "63b4dc6c732fc8bf", "bytes_per_launch": 4555134686},
 }
 
 
